@@ -1,0 +1,378 @@
+"""Pins of the CPU oracle against things other than itself (no GPU).
+
+Routing (token reorganisation, EaaS §3.3; group-shrink compaction, §4.1):
+hand-derived fixtures, a pure-Python comparison sort, invariants.
+FFN + weighted sum (§3.3): a hand-computed fixture, torch's dense SwiGLU for
+the single-expert case, one-hot and dense-mixture special cases, linearity,
+brute force, and the budget of the bf16 intermediate.
+Number formats: torch's bf16 and fp8-e4m3fn casts.
+The planted-mistake tests at the end show that a plausible slip in the oracle
+fails at least one pin.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import eaas_oracle as O
+from paper_2509_17863_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _bits(a):
+    return synth.bf16_bits_from_f32(np.asarray(a, dtype=np.float32))
+
+
+def small_inputs(T=37, H=64, I=32, E=5, k=2, seed=11, mask=0.0, dup=False, zipf=None):
+    """Small random request (any H, I: the oracle has no tiling constraints)."""
+    d = synth.make_inputs(T, H, I, E, k, seed, zipf=zipf)
+    rng = np.random.default_rng(seed + 1000)
+    ids = d["topk_ids"].copy()
+    if mask > 0:
+        m = rng.random(ids.shape) < mask
+        ids[m] = rng.choice(np.array([-1, E, E + 7, -5], dtype=np.int32), size=int(m.sum()))
+    if dup and k > 1:
+        ids[::3, 1] = ids[::3, 0]
+    d["topk_ids"] = ids
+    return d
+
+
+# ----------------------------------------------------------------- routing
+def check_routing_hand(route_fn):
+    for c in _load("routing_hand.json")["cases"]:
+        r = route_fn(np.array(c["topk_ids"], dtype=np.int32), c["E"])
+        for key in ("counts", "offsets", "perm", "inv", "active"):
+            assert r[key].tolist() == c[key], key
+
+
+def test_routing_hand_fixtures():
+    check_routing_hand(O.route_permute)
+
+
+def python_sort_routing(ids, E):
+    flat = [int(v) for v in np.asarray(ids).reshape(-1)]
+    valid = [s for s, e in enumerate(flat) if 0 <= e < E]
+    order = sorted(valid, key=lambda s: (flat[s], s))
+    counts = [sum(1 for s in valid if flat[s] == e) for e in range(E)]
+    offsets = [0]
+    for c in counts:
+        offsets.append(offsets[-1] + c)
+    perm = order + [-1] * (len(flat) - len(order))
+    inv = [-1] * len(flat)
+    for r, s in enumerate(order):
+        inv[s] = r
+    act = [e for e in range(E) if counts[e] > 0]
+    active = [len(act)] + act + [0] * (E - len(act))
+    return dict(counts=counts, offsets=offsets, perm=perm, inv=inv, active=active)
+
+
+@pytest.mark.parametrize("T,E,k,mask,dup", [(1, 1, 1, 0, False), (50, 7, 3, 0.2, True),
+                                            (300, 64, 8, 0.1, False), (17, 3, 5, 0.0, True),
+                                            (40, 1024, 2, 0.3, False)])
+def test_routing_vs_python_sort(T, E, k, mask, dup):
+    rng = np.random.default_rng(T * 7 + E)
+    ids = rng.integers(0, E, size=(T, k)).astype(np.int32)
+    if mask:
+        m = rng.random(ids.shape) < mask
+        ids[m] = -1
+    if dup:
+        ids[::2, 0] = ids[::2, -1]
+    r = O.route_permute(ids, E)
+    ref = python_sort_routing(ids, E)
+    for key in ref:
+        assert r[key].tolist() == ref[key], key
+
+
+@pytest.mark.parametrize("name", list(synth.WORKLOADS))
+def test_routing_invariants_workloads(name):
+    d = synth.make_workload(name, weights=False)
+    E, T, k = d["E"], d["T"], d["k"]
+    r = O.route_permute(d["topk_ids"], E)
+    R = T * k
+    assert r["offsets"][E] == R  # nothing masked in the named workloads
+    assert np.array_equal(np.sort(r["perm"]), np.arange(R))  # bijection
+    assert np.array_equal(r["inv"][r["perm"]], np.arange(R))
+    assert np.array_equal(r["counts"], np.bincount(d["topk_ids"].ravel(), minlength=E))
+    assert np.all(np.diff(r["offsets"]) >= 0) and r["counts"].sum() == R
+    act = r["active"][1: 1 + r["active"][0]]
+    assert np.all(np.diff(act) > 0) and np.all(r["counts"][act] > 0)
+    assert r["active"][0] == np.count_nonzero(r["counts"])
+    ids_flat = d["topk_ids"].ravel()
+    # rows of each expert hold that expert's slots, ascending
+    for e in act:
+        seg = r["perm"][r["offsets"][e]: r["offsets"][e + 1]]
+        assert np.all(ids_flat[seg] == e) and np.all(np.diff(seg) > 0)
+
+
+# ----------------------------------------------------------------- numbers
+def test_bf16_rne_matches_torch():
+    rng = np.random.default_rng(3)
+    a = np.concatenate([rng.standard_normal(20000).astype(np.float32) * 10,
+                        np.array([0.0, -0.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 1.0 + 2 ** -9,
+                                  -(1.0 + 2 ** -8), 3.0e38, 1e-40, -1e-42, np.inf, -np.inf],
+                                 dtype=np.float32)])
+    ours = O.f32_to_bf16_rne(a)
+    ref = torch.from_numpy(a).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
+    assert np.isnan(O.bf16_to_f32(O.f32_to_bf16_rne(np.array([np.nan], np.float32))))[0]
+    assert np.array_equal(O.bf16_to_f32(ref), torch.from_numpy(ref.view(np.int16)).view(
+        torch.bfloat16).float().numpy())
+
+
+def test_e4m3fn_decode_all_codes_matches_torch():
+    codes = np.arange(256, dtype=np.uint8)
+    ours = O.e4m3fn_to_f32(codes)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).float().numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(ours), nan)
+    assert np.array_equal(ours[~nan], ref[~nan])
+    assert ours[0x7E] == 448.0 and ours[0x01] == 2.0 ** -9 and ours[0x08] == 2.0 ** -6
+
+
+def test_dequantize_block_indexing():
+    # non-square block grid: a transposed or swapped scale index changes values
+    q = np.full((256, 384), 0x38, dtype=np.uint8)  # 0x38 = 1.0 in e4m3fn
+    s = np.arange(1, 7, dtype=np.float32).reshape(2, 3)
+    w = O.dequantize_blocks(q, s)
+    for bi in range(2):
+        for bj in range(3):
+            blk = w[bi * 128:(bi + 1) * 128, bj * 128:(bj + 1) * 128]
+            assert np.all(blk == s[bi, bj])
+
+
+def test_fp8_generator_roundtrip_error_bound():
+    rng = np.random.default_rng(5)
+    w = rng.standard_normal((256, 256)).astype(np.float32) * 0.05
+    q, s = synth.fp8e4m3_quantize_blocks(w)
+    back = O.dequantize_blocks(q, s)
+    # e4m3 has 3 mantissa bits: relative rounding error <= 2^-4 for normals,
+    # absolute error <= s * 2^-10 in the subnormal range
+    srep = np.repeat(np.repeat(s, 128, 0), 128, 1)
+    err = np.abs(back - w)
+    assert np.all(err <= np.maximum(np.abs(w) * 2.0 ** -4, srep * 2.0 ** -10) * 1.0001)
+
+
+# ----------------------------------------------------------------- FFN
+def test_silu_closed_forms():
+    g = np.array([0.0, 30.0, -30.0, 1.0, -1.0], np.float32)
+    h = O.bf16_to_f32(O.silu_mul_to_bf16(g, np.ones_like(g)))
+    assert h[0] == 0.0 and h[1] == 30.0 and abs(h[2]) < 1e-10
+    # silu(x) - silu(-x) = x
+    assert abs((h[3] - h[4]) - 1.0) < 2 ** -7
+
+
+def hand_ffn_inputs():
+    c = _load("ffn_hand.json")
+    d = dict(T=1, H=c["H"], I=c["I"], E=c["E"], k=c["k"], wdtype="bf16",
+             x=_bits(c["x"]), topk_ids=np.array(c["topk_ids"], np.int32),
+             topk_weights=np.array(c["topk_weights"], np.float32),
+             w_gate_up=_bits(c["w_gate_up"]), w_gate_up_scale=None,
+             w_down=_bits(c["w_down"]), w_down_scale=None)
+    return d, c
+
+
+def check_ffn_hand(fwd_fn):
+    d, c = hand_ffn_inputs()
+    res = fwd_fn(d)
+    assert np.array_equal(res["out"], np.array(c["out"]))
+
+
+def test_ffn_hand_fixture():
+    d, c = hand_ffn_inputs()
+    res = O.expert_forward(d)
+    r = res["routing"]
+    h_rows = O.bf16_to_f32(res["h"])
+    # rows are experts 0 then 1
+    assert r["perm"].tolist() == [0, 1]
+    assert np.array_equal(h_rows, np.array(c["h"], np.float32))
+    check_ffn_hand(O.expert_forward)
+
+
+def torch_dense_swiglu(x_bits, wgu_bits, wd_bits, I):
+    """Single expert, by torch ops: F.silu on fp32 gate, bf16 cast of h, fp64 down."""
+    x = torch.from_numpy(O.bf16_to_f32(x_bits)).double()
+    wgu = torch.from_numpy(O.bf16_to_f32(wgu_bits)).double()
+    wd = torch.from_numpy(O.bf16_to_f32(wd_bits)).double()
+    g = torch.nn.functional.linear(x, wgu[:I]).float()
+    u = torch.nn.functional.linear(x, wgu[I:]).float()
+    h = (torch.nn.functional.silu(g) * u).to(torch.bfloat16).double()
+    return torch.nn.functional.linear(h, wd).numpy()
+
+
+def check_dense_single_expert(fwd_fn):
+    d = synth.make_inputs(41, 96, 64, 1, 1, seed=7)
+    d["topk_weights"] = np.ones_like(d["topk_weights"])
+    out = fwd_fn(d)["out"]
+    ref = torch_dense_swiglu(d["x"], d["w_gate_up"][0], d["w_down"][0], d["I"])
+    rms = np.sqrt((ref ** 2).mean())
+    # torch's silu and numpy's exp may differ in the last fp32 bit, which can
+    # flip a bf16 rounding of h: allow a few such flips, nothing more
+    assert np.abs(out - ref).max() <= 2e-3 * rms
+
+
+def test_dense_single_expert_matches_torch():
+    check_dense_single_expert(O.expert_forward)
+
+
+def check_one_hot(fwd_fn):
+    d = small_inputs(T=29, E=4, k=3, seed=5)
+    d["topk_weights"] = np.zeros_like(d["topk_weights"])
+    d["topk_weights"][:, 0] = 1.0
+    out = fwd_fn(d)["out"]
+    for t in range(d["T"]):
+        e = int(d["topk_ids"][t, 0])
+        ref = torch_dense_swiglu(d["x"][t: t + 1], d["w_gate_up"][e], d["w_down"][e], d["I"])
+        assert np.abs(out[t] - ref[0]).max() <= 2e-3 * np.sqrt((ref ** 2).mean()) + 1e-12
+
+
+def test_one_hot_weights_select_first_expert():
+    check_one_hot(O.expert_forward)
+
+
+def check_dense_mixture(fwd_fn):
+    E = 3
+    d = small_inputs(T=23, E=E, k=E, seed=9)
+    out = fwd_fn(d)["out"]
+    ref = np.zeros_like(out)
+    for e in range(E):
+        ye = torch_dense_swiglu(d["x"], d["w_gate_up"][e], d["w_down"][e], d["I"])
+        we = np.where(d["topk_ids"] == e, d["topk_weights"], 0.0).sum(1)
+        ref += we[:, None].astype(np.float64) * ye
+    assert np.abs(out - ref).max() <= 2e-3 * np.sqrt((ref ** 2).mean())
+
+
+def test_k_equals_E_is_dense_mixture():
+    check_dense_mixture(O.expert_forward)
+
+
+def test_linearity_in_weights_exact():
+    d = small_inputs(seed=13, mask=0.2)
+    a = O.expert_forward(d)["out"]
+    d2 = dict(d, topk_weights=d["topk_weights"] * np.float32(2.0))
+    b = O.expert_forward(d2)["out"]
+    assert np.array_equal(b, 2.0 * a)
+
+
+@pytest.mark.parametrize("kw", [dict(), dict(mask=0.3), dict(dup=True, k=3),
+                                dict(E=1, k=1), dict(T=5, E=9, k=4, mask=0.5),
+                                dict(zipf=3.0, E=16, k=2, T=60)])
+def test_grouped_matches_brute_force(kw):
+    d = small_inputs(**kw)
+    res = O.expert_forward(d)
+    bf = O.brute_force_tokens(d, range(d["T"]))
+    rms = np.sqrt((bf ** 2).mean()) or 1.0
+    assert np.abs(res["out"] - bf).max() <= 1e-12 * rms
+
+
+def test_masked_token_is_zero_and_masked_slots_skipped():
+    d = small_inputs(T=12, E=4, k=2, seed=21)
+    d["topk_ids"][3] = [-1, 4]
+    d["topk_ids"][5, 1] = 17
+    res = O.expert_forward(d)
+    assert np.all(res["out"][3] == 0.0)
+    d2 = dict(d, topk_ids=d["topk_ids"].copy(), topk_weights=d["topk_weights"].copy())
+    d2["topk_ids"][5, 1] = d["topk_ids"][5, 0]
+    d2["topk_weights"][5, 1] = 0.0
+    assert np.allclose(O.expert_forward(d2)["out"][5], res["out"][5], rtol=0, atol=1e-14)
+
+
+def test_token_permutation_equivariance():
+    d = small_inputs(T=40, E=6, k=2, seed=4, mask=0.1)
+    p = np.random.default_rng(0).permutation(d["T"])
+    a = O.expert_forward(d)["out"]
+    b = O.expert_forward(O.sub_batch(d, p))["out"]
+    assert np.abs(b - a[p]).max() <= 1e-12 * np.sqrt((a ** 2).mean())
+
+
+def test_bf16_intermediate_within_budget():
+    # the exact fp64 SwiGLU (no bf16 h) differs from the oracle by well under
+    # the 2e-2 x RMS acceptance bound at the tiny workload
+    d = synth.make_workload("tiny")
+    res = O.expert_forward(d)
+    exact = O.brute_force_tokens(d, range(d["T"]), mirror_h=False)
+    rms = np.sqrt((exact ** 2).mean())
+    assert np.abs(res["out"] - exact).max() <= 1e-2 * rms
+
+
+def test_fp8_weights_equal_dequantised_bf16_path():
+    d = synth.make_inputs(20, 256, 128, 3, 2, seed=8, wdtype="fp8")
+    res8 = O.expert_forward(d)
+    wgu, wdn = O.weights_f32(d)
+    resf = O.expert_forward(d, weights=(wgu, wdn))
+    assert np.array_equal(res8["out"], resf["out"])
+    # dequantised values are exact products q*s
+    q = O.e4m3fn_to_f32(d["w_gate_up"][1, :128, :128]).astype(np.float64)
+    assert np.array_equal(wgu[1, :128, :128].astype(np.float64),
+                          (q * d["w_gate_up_scale"][1, 0, 0]).astype(np.float32).astype(np.float64))
+
+
+# ----------------------------------------------------------------- planted mistakes
+def _mutants(monkeypatch):
+    """Each entry plants one plausible slip into a copy of the oracle's logic."""
+    real_route = O.route_permute
+    real_silu = O.silu_mul_to_bf16
+    real_combine = O.unpermute_combine
+
+    def route_unstable(ids, E):
+        r = real_route(ids, E)
+        off = r["offsets"]
+        for e in range(E):
+            seg = r["perm"][off[e]:off[e + 1]]
+            r["perm"][off[e]:off[e + 1]] = seg[::-1]
+        r["inv"][r["perm"][: off[E]]] = np.arange(off[E], dtype=np.int32)
+        return r
+
+    def route_active_unsorted(ids, E):
+        r = real_route(ids, E)
+        n = r["active"][0]
+        r["active"][1:1 + n] = r["active"][1:1 + n][::-1]
+        return r
+
+    def silu_swapped(G, U):
+        return real_silu(U, G)
+
+    def silu_sign(G, U):
+        return real_silu(-G, U)
+
+    def combine_drop_last(y, routing, w):
+        w2 = w.copy()
+        w2[:, -1] = 0
+        return real_combine(y, routing, w2)
+
+    def combine_wrong_weight(y, routing, w):
+        return real_combine(y, routing, w[:, ::-1].copy())
+
+    return [("route_permute", route_unstable), ("route_permute", route_active_unsorted),
+            ("silu_mul_to_bf16", silu_swapped), ("silu_mul_to_bf16", silu_sign),
+            ("unpermute_combine", combine_drop_last), ("unpermute_combine", combine_wrong_weight)]
+
+
+def _all_pins():
+    yield lambda: check_routing_hand(O.route_permute)
+    yield lambda: check_ffn_hand(O.expert_forward)
+    yield lambda: check_dense_single_expert(O.expert_forward)
+    yield lambda: check_one_hot(O.expert_forward)
+    yield lambda: check_dense_mixture(O.expert_forward)
+
+
+@pytest.mark.parametrize("idx", range(6))
+def test_planted_mistake_is_caught(monkeypatch, idx):
+    name, fn = _mutants(monkeypatch)[idx]
+    monkeypatch.setattr(O, name, fn)
+    caught = 0
+    for pin in _all_pins():
+        try:
+            pin()
+        except AssertionError:
+            caught += 1
+    assert caught >= 1, f"no pin caught the planted mistake in {name}"
