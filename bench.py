@@ -1,0 +1,176 @@
+"""Benchmark of one expert server's forward step on one MI355X.
+
+A step is one eaas_expert_forward over one batch of the named synthetic
+workload (routing, grouped gate/up GEMM + SiLU*mul, grouped down GEMM with the
+weighted epilogue, combine), inputs resident in HBM.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def cpu_threads() -> int:
+    n = len(os.sched_getaffinity(0))
+    omp = os.environ.get("OMP_NUM_THREADS")
+    return min(n, int(omp)) if omp and omp.isdigit() else n
+
+
+def algorithmic(d: dict, counts: np.ndarray) -> dict:
+    """Algorithmic flops and bytes of the step and of each GEMM kernel."""
+    T, H, I, E, k = d["T"], d["H"], d["I"], d["E"], d["k"]
+    R = int(counts.sum())
+    n_act = int((counts > 0).sum())
+    wb = 1 if d["wdtype"] == "fp8" else 2
+    sgu = (2 * I // 128) * (H // 128) * 4 if wb == 1 else 0
+    sdn = (H // 128) * (I // 128) * 4 if wb == 1 else 0
+    gu_bytes = n_act * (2 * I * H * wb + sgu) + T * H * 2 + R * I * 2 + R * 4
+    dn_bytes = n_act * (H * I * wb + sdn) + R * I * 2 + T * H * 2 + R * 4
+    return dict(flops=6.0 * R * H * I, gu_flops=4.0 * R * H * I, dn_flops=2.0 * R * H * I,
+                gu_bytes=gu_bytes, dn_bytes=dn_bytes,
+                bytes=gu_bytes + dn_bytes - R * I * 2 * 0 + T * k * 4)
+
+
+def cpu_baseline(d: dict, target_s: float = 12.0) -> dict:
+    """The oracle, untuned, on a bounded token sample (weights pre-converted
+    to fp64 outside the timed region)."""
+    from oracle import eaas_oracle as O
+
+    E = d["E"]
+    w64 = ([], [])
+    for e in range(E):
+        wg, wu, wd = O.expert_weights_f64(d, e)
+        w64[0].append(np.concatenate([wg, wu]))
+        w64[1].append(wd)
+    rng = np.random.default_rng(7)
+
+    def run(n):
+        tok = np.sort(rng.choice(d["T"], size=n, replace=False))
+        sub = O.sub_batch(d, tok)
+        t0 = time.perf_counter()
+        O.expert_forward(sub, weights=w64)
+        return time.perf_counter() - t0
+
+    n = min(d["T"], 64)
+    t = run(n)
+    if t < target_s and n < d["T"]:
+        n = int(min(d["T"], max(n, n * target_s / max(t, 1e-3))))
+        t = run(n)
+    return {"value": n / t, "unit": "tokens/s", "cores": cpu_threads(), "kind": "oracle",
+            "sample": f"{n} of {d['T']} tokens of the same batch (oracle expert_forward on the "
+                      f"sub-batch, fp64 BLAS, {t:.1f} s; weights converted to fp64 beforehand)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mixtral")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one expert server on one GPU; --gpus {args.gpus} is not "
+              "supported (the step has no cross-GPU exchange; experts shard by server)",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    from oracle import eaas_oracle as O
+    from paper_2509_17863_amd import eaas, synth
+    from paper_2509_17863_amd.device_io import to_device
+
+    assert torch.cuda.is_available(), "no GPU"
+    wl = synth.WORKLOADS[args.workload]
+    d = synth.make_workload(args.workload)
+    dev = to_device(d)
+    T, H, I, E, k = d["T"], d["H"], d["I"], d["E"], d["k"]
+    wdt = eaas.EAAS_FP8_E4M3 if d["wdtype"] == "fp8" else eaas.EAAS_BF16
+    ws = eaas.alloc_workspace(T, H, I, E, k, wdt)
+    out = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
+    counts = np.bincount(d["topk_ids"].ravel()[d["topk_ids"].ravel() >= 0], minlength=E)
+    alg = algorithmic(d, counts)
+
+    stream = torch.cuda.current_stream()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+
+    def step(ev=None):
+        if ev is None:
+            eaas.eaas_expert_forward(dev["x"], dev["topk_ids"], dev["topk_weights"],
+                                     dev["w_gate_up"], dev["w_down"], out, ws,
+                                     dev["w_gate_up_scale"], dev["w_down_scale"])
+        else:
+            eaas.eaas_expert_forward_profiled(dev["x"], dev["topk_ids"], dev["topk_weights"],
+                                              dev["w_gate_up"], dev["w_down"], out, ws,
+                                              dev["w_gate_up_scale"], dev["w_down_scale"],
+                                              events=ev)
+
+    for ev in evs:  # create the events before the timed region
+        for e in ev:
+            e.record(stream)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / args.steps
+
+    def mean_ms(a, b):
+        return float(np.mean([evs[i][a].elapsed_time(evs[i][b]) for i in range(args.steps)]))
+
+    t_route, t_gu, t_dn, t_comb = mean_ms(0, 1), mean_ms(1, 2), mean_ms(2, 3), mean_ms(3, 4)
+    t_step_ev = mean_ms(0, 4)
+    hbm_bound = d["wdtype"] == "fp8"
+    if hbm_bound:
+        achieved = alg["gu_bytes"] / (t_gu * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+    else:
+        achieved = alg["gu_flops"] / (t_gu * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None}
+    roof["kernel"] = "grouped_gemm_kernel<gate/up>"
+    res = {
+        "metric": "expert-FFN tokens/s",
+        "value": round(T / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.workload, "T": T, "H": H, "I": I, "E": E, "k": k,
+                   "weights": d["wdtype"], "seed": wl.seed, "zipf": wl.zipf,
+                   "active_experts": int((counts > 0).sum()), "parallelism": "none (1 GPU)"},
+        "step_tflops": round(alg["flops"] / (ms * 1e-3) / 1e12, 1),
+        "step_frac_bf16_peak": round(alg["flops"] / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "kernels_ms": {"route": round(t_route, 4), "gate_up": round(t_gu, 4),
+                       "down": round(t_dn, 4), "combine": round(t_comb, 4),
+                       "step_events": round(t_step_ev, 4)},
+        "down_tflops": round(alg["dn_flops"] / (t_dn * 1e-3) / 1e12, 1),
+        "roofline": roof,
+    }
+    if hbm_bound:
+        res["step_hbm_gbs"] = round((alg["gu_bytes"] + alg["dn_bytes"]) / (ms * 1e-3) / 1e9, 1)
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(d)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

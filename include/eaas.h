@@ -1,0 +1,179 @@
+/*
+ * eaas.h -- C ABI of one stateless expert server's forward step on gfx950.
+ *
+ * The operation (EaaS, §3.3 "Asynchronous Server Operation", and Fig. 5): the
+ * server takes a batch of ready requests, reorganises the tokens by expert,
+ * runs the grouped expert computation, and writes back for every token the
+ * weighted sum of its experts' outputs.  The request payload (§3.2 "Data
+ * Payload") carries the hidden states, an expert id per token slot and the
+ * router score used for weighting; the header carries the batch size (§3.2
+ * "Header").  The server is stateless (§2.4, §3.3): nothing survives between
+ * calls, so every call is a pure function of its arguments.
+ *
+ * Symbols: T tokens (header batch_size), H hidden size, I expert intermediate
+ * size, E resident experts on this server, k expert slots per token,
+ * R = T*k slots.  Slot s = t*k + j.  A slot is valid iff 0 <= topk_ids[s] < E;
+ * other ids (experts hosted by other servers) are skipped, not errors.
+ *
+ * Expert FFN (the paper names only "expert computations"; this library
+ * implements the SwiGLU form without bias):
+ *     y_e(x) = W_down[e] . ( silu(W_gate[e] . x) * (W_up[e] . x) )
+ * with W_gate_up[e] = [W_gate[e]; W_up[e]] stacked by rows (gate rows [0,I),
+ * up rows [I,2I)), W_gate_up[E,2I,H] and W_down[E,H,I], both [out,in]
+ * row-major.  Accumulation is fp32; the intermediate h is rounded once to
+ * bf16 (round to nearest even); the weighted sum is fp32, summed over valid
+ * slots in ascending j starting from +0.
+ *
+ * Weights are bf16, or OCP fp8 e4m3fn with one fp32 scale per 128x128 block
+ * of each expert matrix (W = q * s): scale arrays [E,2I/128,H/128] and
+ * [E,H/128,I/128], row-major.
+ *
+ * Conventions for every entry point:
+ *   - All array pointers are DEVICE pointers owned by the caller; the shape
+ *     descriptor and the routing descriptor themselves live in host memory.
+ *   - The library never allocates, frees or synchronises.  Scratch memory is
+ *     the caller's workspace `ws` of at least eaas_workspace_bytes() bytes,
+ *     256-byte aligned.  Its contents are undefined between calls.
+ *   - `stream` is a hipStream_t passed as void* (NULL = null stream).  All work
+ *     is enqueued on it with no host synchronisation and no device-to-host
+ *     readback, so calls can be captured in a hipGraph.
+ *   - Arguments are validated on the host before anything is enqueued; on any
+ *     error a negative status is returned and nothing is enqueued.  T = 0 is
+ *     a valid empty batch: EAAS_OK, nothing enqueued, outputs left untouched
+ *     (pointers may then be NULL).  Device arrays must be 16-byte aligned
+ *     (EAAS_ERR_INVALID_ARG otherwise).
+ *   - Calls are re-entrant; concurrent calls must use distinct workspaces and
+ *     outputs.
+ *   - NaN and Inf in the data propagate; they are not errors.
+ */
+#ifndef EAAS_H
+#define EAAS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct eaas_shape {
+  int32_t T; /* tokens in the batch (>= 0)                              */
+  int32_t H; /* hidden size, multiple of 128                             */
+  int32_t I; /* expert intermediate size, multiple of 128                */
+  int32_t E; /* resident experts, 1..1024                                */
+  int32_t k; /* slots per token, 1..64                                   */
+} eaas_shape;
+
+enum eaas_status {
+  EAAS_OK = 0,
+  EAAS_ERR_INVALID_ARG = -1, /* null pointer, negative size, bad dtype, overlap */
+  EAAS_ERR_UNSUPPORTED = -2, /* H or I not a multiple of 128, E > 1024, k > 64,
+                                T*k >= 2^31 or sizes past 32-bit row indexing */
+  EAAS_ERR_WORKSPACE = -3,   /* ws NULL or smaller than eaas_workspace_bytes */
+  EAAS_ERR_HIP = -4          /* a kernel launch was rejected by the runtime  */
+};
+
+enum eaas_dtype {
+  EAAS_BF16 = 0,     /* bfloat16 bit patterns (uint16)                    */
+  EAAS_FP8_E4M3 = 1, /* OCP fp8 e4m3fn bit patterns (uint8), weights only */
+  EAAS_FP32 = 2      /* IEEE binary32, outputs only                       */
+};
+
+/*
+ * Routing of a batch: the token reorganisation of §3.3 plus the compacted
+ * active-expert list of the group-shrink prefix scan (§4.1).  Device arrays:
+ *   counts [E]    valid slots per expert
+ *   offsets[E+1]  exclusive prefix sum of counts; offsets[E] = valid slots
+ *   perm   [R]    row r -> slot s; rows are grouped by expert in ascending
+ *                 expert id and, inside an expert, in ascending slot order
+ *                 (the unique stable counting sort); rows >= offsets[E] hold -1
+ *   inv    [R]    slot s -> row, or -1 for an invalid slot
+ *   active [E+1]  active[0] = number of experts with counts > 0, then those
+ *                 experts in ascending order, then zeros
+ */
+typedef struct eaas_routing {
+  int32_t *counts;
+  int32_t *offsets;
+  int32_t *perm;
+  int32_t *inv;
+  int32_t *active;
+} eaas_routing;
+
+/* Bytes of workspace that every entry point below accepts for this shape and
+ * weight dtype (the maximum over the entry points).  Returns 0 for a shape the
+ * library rejects. */
+size_t eaas_workspace_bytes(const eaas_shape *s, int w_dtype);
+
+/* Token reorganisation + group-shrink (§3.3 Fig. 5, §4.1).
+ *   topk_ids [T,k] int32   expert id per slot (payload `expert_id`, §3.2)
+ *   r                      all five arrays written, bit-exact and deterministic
+ * Needs ws of eaas_workspace_bytes(s, EAAS_BF16) bytes. */
+int eaas_route_permute(const eaas_shape *s, const int32_t *topk_ids,
+                       const eaas_routing *r, void *ws, size_t ws_bytes,
+                       void *stream);
+
+/* Grouped expert FFN over the reorganised rows (§3.3 "grouped GEMM").
+ *   x          [T,H] bf16 hidden states (payload, §3.2)
+ *   r          routing produced by eaas_route_permute for the same ids
+ *   w_gate_up  [E,2I,H] bf16 or fp8; w_gate_up_scale [E,2I/128,H/128] fp32
+ *              for fp8, ignored (may be NULL) for bf16
+ *   w_down     [E,H,I]  bf16 or fp8; w_down_scale [E,H/128,I/128] likewise
+ *   y_perm     [R,H] fp32 output: row r = y_{e(r)}(x[perm[r]/k]), unweighted;
+ *              rows >= offsets[E] are left untouched
+ * Only experts listed in r->active are read. */
+int eaas_expert_ffn_grouped(const eaas_shape *s, const void *x,
+                            const eaas_routing *r, const void *w_gate_up,
+                            const float *w_gate_up_scale, const void *w_down,
+                            const float *w_down_scale, int w_dtype,
+                            float *y_perm, void *ws, size_t ws_bytes,
+                            void *stream);
+
+/* Weighted sum of expert outputs back into token order (§3.3 "the weighted sum
+ * of expert outputs", weights = router_score of §3.2).
+ *   out[t,:] = sum over ascending j with valid slot t*k+j of
+ *              fp32(topk_weights[t,j] * y_perm[inv[t*k+j],:]), from +0
+ *   out        [T,H] bf16 (round to nearest even of the fp32 sum) or fp32;
+ *              tokens with no valid slot get zeros. */
+int eaas_unpermute_combine(const eaas_shape *s, const float *y_perm,
+                           const eaas_routing *r, const float *topk_weights,
+                           void *out, int out_dtype, void *stream);
+
+/* The whole step: route_permute, grouped FFN and weighted combine in one call,
+ * result bitwise equal to calling the three entry points above in sequence.
+ *   r      optional (NULL: routing lives in the workspace); when given it is
+ *          written as by eaas_route_permute
+ *   out    [T,H] bf16 or fp32.  out == x (exactly, bf16 out) is allowed: the
+ *          result is written back into the request payload in place (§3.3);
+ *          any other overlap of out with x is EAAS_ERR_INVALID_ARG. */
+int eaas_expert_forward(const eaas_shape *s, const void *x,
+                        const int32_t *topk_ids, const float *topk_weights,
+                        const void *w_gate_up, const float *w_gate_up_scale,
+                        const void *w_down, const float *w_down_scale,
+                        int w_dtype, void *out, int out_dtype,
+                        const eaas_routing *r, void *ws, size_t ws_bytes,
+                        void *stream);
+
+/* eaas_expert_forward, plus timing marks for measurement: events[0..4] are
+ * hipEvent_t handles (passed as void*, NULL entries skipped) recorded on
+ * `stream` before routing, before the gate/up GEMM, before the down GEMM,
+ * before the combine and after it.  events itself may be NULL.  Same kernels,
+ * same results as eaas_expert_forward. */
+int eaas_expert_forward_profiled(const eaas_shape *s, const void *x,
+                                 const int32_t *topk_ids,
+                                 const float *topk_weights,
+                                 const void *w_gate_up,
+                                 const float *w_gate_up_scale,
+                                 const void *w_down, const float *w_down_scale,
+                                 int w_dtype, void *out, int out_dtype,
+                                 const eaas_routing *r, void *ws,
+                                 size_t ws_bytes, void *stream,
+                                 void *const *events);
+
+/* Static, human-readable name of a status code. */
+const char *eaas_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EAAS_H */

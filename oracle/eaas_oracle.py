@@ -101,8 +101,8 @@ def expert_weights_f64(inp: dict, e: int, weights=None):
     else:
         wgu = dequantize_blocks(inp["w_gate_up"][e], inp["w_gate_up_scale"][e])
         wdn = dequantize_blocks(inp["w_down"][e], inp["w_down_scale"][e])
-    wgu = wgu.astype(np.float64)
-    return wgu[:I], wgu[I:], wdn.astype(np.float64)
+    wgu = np.asarray(wgu, dtype=np.float64)
+    return wgu[:I], wgu[I:], np.asarray(wdn, dtype=np.float64)
 
 
 def sub_batch(inp: dict, tokens) -> dict:

@@ -1,0 +1,230 @@
+// C ABI of the expert-server forward step: host-side validation, workspace
+// layout and kernel enqueueing.  No allocation, no synchronisation, no
+// device-to-host traffic: every entry point only enqueues work on `stream`.
+#include <limits.h>
+#include <stdint.h>
+
+#include "common.h"
+#include "internal.h"
+
+namespace {
+
+using namespace eaas;
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct WsLayout {
+  size_t hist, counts, offsets, perm, inv, active, h, stage, total;
+};
+
+WsLayout layout(const eaas_shape& s) {
+  const size_t R = (size_t)s.T * s.k;
+  WsLayout L{};
+  size_t o = 0;
+  L.hist = o;    o = align_up(o + (size_t)route_blocks((int)R) * s.E * 4);
+  L.counts = o;  o = align_up(o + (size_t)s.E * 4);
+  L.offsets = o; o = align_up(o + (size_t)(s.E + 1) * 4);
+  L.perm = o;    o = align_up(o + R * 4);
+  L.inv = o;     o = align_up(o + R * 4);
+  L.active = o;  o = align_up(o + (size_t)(s.E + 1) * 4);
+  L.h = o;       o = align_up(o + R * s.I * 2);
+  L.stage = o;   o = align_up(o + R * s.H * 4);
+  L.total = o;
+  return L;
+}
+
+int check_shape(const eaas_shape* s) {
+  if (!s) return EAAS_ERR_INVALID_ARG;
+  if (s->T < 0 || s->H <= 0 || s->I <= 0 || s->E <= 0 || s->k <= 0) return EAAS_ERR_INVALID_ARG;
+  if (s->H % 128 || s->I % 128 || s->E > kMaxExperts || s->k > kMaxTopK) return EAAS_ERR_UNSUPPORTED;
+  const long long R = (long long)s->T * s->k;
+  // 32-bit element offsets inside the kernels
+  if (R > INT_MAX || (long long)s->T * s->H > INT_MAX || R * s->I > INT_MAX ||
+      4LL * s->I * s->H > INT_MAX)
+    return EAAS_ERR_UNSUPPORTED;
+  return EAAS_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool routing_ok(const eaas_routing* r) {
+  return r && r->counts && r->offsets && r->perm && r->inv && r->active &&
+         aligned16(r->perm) && aligned16(r->inv);
+}
+
+bool weights_ok(const void* wgu, const float* sgu, const void* wd, const float* sd, int w_dtype) {
+  if (!wgu || !wd || !aligned16(wgu) || !aligned16(wd)) return false;
+  if (w_dtype == EAAS_BF16) return true;
+  if (w_dtype == EAAS_FP8_E4M3) return sgu && sd;
+  return false;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? EAAS_OK : EAAS_ERR_HIP; }
+
+eaas_routing ws_routing(char* base, const WsLayout& L) {
+  eaas_routing r;
+  r.counts = reinterpret_cast<int32_t*>(base + L.counts);
+  r.offsets = reinterpret_cast<int32_t*>(base + L.offsets);
+  r.perm = reinterpret_cast<int32_t*>(base + L.perm);
+  r.inv = reinterpret_cast<int32_t*>(base + L.inv);
+  r.active = reinterpret_cast<int32_t*>(base + L.active);
+  return r;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t eaas_workspace_bytes(const eaas_shape* s, int w_dtype) {
+  if (check_shape(s) != EAAS_OK) return 0;
+  if (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3) return 0;
+  return layout(*s).total;
+}
+
+int eaas_route_permute(const eaas_shape* s, const int32_t* topk_ids, const eaas_routing* r,
+                       void* ws, size_t ws_bytes, void* stream) {
+  int st = check_shape(s);
+  if (st != EAAS_OK) return st;
+  if (s->T == 0) return EAAS_OK;
+  if (!topk_ids || !routing_ok(r)) return EAAS_ERR_INVALID_ARG;
+  const WsLayout L = layout(*s);
+  if (!ws || !aligned16(ws) || ws_bytes < L.total) return EAAS_ERR_WORKSPACE;
+  char* base = static_cast<char*>(ws);
+  return hip_status(launch_route_permute(topk_ids, s->T * s->k, s->E, *r,
+                                         reinterpret_cast<int32_t*>(base + L.hist),
+                                         reinterpret_cast<hipStream_t>(stream)));
+}
+
+int eaas_expert_ffn_grouped(const eaas_shape* s, const void* x, const eaas_routing* r,
+                            const void* w_gate_up, const float* w_gate_up_scale,
+                            const void* w_down, const float* w_down_scale, int w_dtype,
+                            float* y_perm, void* ws, size_t ws_bytes, void* stream) {
+  int st = check_shape(s);
+  if (st != EAAS_OK) return st;
+  if (s->T == 0) return EAAS_OK;
+  if (!x || !aligned16(x) || !routing_ok(r) || !y_perm || !aligned16(y_perm) ||
+      !weights_ok(w_gate_up, w_gate_up_scale, w_down, w_down_scale, w_dtype))
+    return EAAS_ERR_INVALID_ARG;
+  const WsLayout L = layout(*s);
+  if (!ws || !aligned16(ws) || ws_bytes < L.total) return EAAS_ERR_WORKSPACE;
+  char* base = static_cast<char*>(ws);
+  FfnArgs a{};
+  a.T = s->T; a.H = s->H; a.I = s->I; a.E = s->E; a.k = s->k;
+  a.x = static_cast<const uint16_t*>(x);
+  a.perm = r->perm;
+  a.offsets = r->offsets;
+  a.active = r->active;
+  a.w_gate_up = w_gate_up;
+  a.s_gate_up = w_gate_up_scale;
+  a.w_down = w_down;
+  a.s_down = w_down_scale;
+  a.fp8 = w_dtype == EAAS_FP8_E4M3;
+  a.h = reinterpret_cast<uint16_t*>(base + L.h);
+  a.y = y_perm;
+  a.topk_weights = nullptr;
+  a.epilogue = kDownPlain;
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = launch_gate_up(a, hs);
+  if (e == hipSuccess) e = launch_down(a, hs);
+  return hip_status(e);
+}
+
+int eaas_unpermute_combine(const eaas_shape* s, const float* y_perm, const eaas_routing* r,
+                           const float* topk_weights, void* out, int out_dtype, void* stream) {
+  int st = check_shape(s);
+  if (st != EAAS_OK) return st;
+  if (s->T == 0) return EAAS_OK;
+  if (!y_perm || !aligned16(y_perm) || !routing_ok(r) || !topk_weights || !out ||
+      !aligned16(out) || (out_dtype != EAAS_BF16 && out_dtype != EAAS_FP32))
+    return EAAS_ERR_INVALID_ARG;
+  return hip_status(launch_combine(y_perm, r->inv, topk_weights, s->T, s->H, s->k, false, out,
+                                   out_dtype == EAAS_FP32, reinterpret_cast<hipStream_t>(stream)));
+}
+
+int eaas_expert_forward_profiled(const eaas_shape* s, const void* x, const int32_t* topk_ids,
+                                 const float* topk_weights, const void* w_gate_up,
+                                 const float* w_gate_up_scale, const void* w_down,
+                                 const float* w_down_scale, int w_dtype, void* out,
+                                 int out_dtype, const eaas_routing* r, void* ws,
+                                 size_t ws_bytes, void* stream, void* const* events) {
+  int st = check_shape(s);
+  if (st != EAAS_OK) return st;
+  if (s->T == 0) return EAAS_OK;
+  if (!x || !aligned16(x) || !topk_ids || !topk_weights || !out || !aligned16(out) ||
+      (out_dtype != EAAS_BF16 && out_dtype != EAAS_FP32) ||
+      !weights_ok(w_gate_up, w_gate_up_scale, w_down, w_down_scale, w_dtype) ||
+      (r && !routing_ok(r)))
+    return EAAS_ERR_INVALID_ARG;
+  // out may alias x exactly (bf16 write-back into the payload), nothing else
+  const size_t xb = (size_t)s->T * s->H * 2;
+  const size_t ob = (size_t)s->T * s->H * (out_dtype == EAAS_FP32 ? 4 : 2);
+  const uintptr_t xp = (uintptr_t)x, op = (uintptr_t)out;
+  if (op == xp) {
+    if (out_dtype != EAAS_BF16) return EAAS_ERR_INVALID_ARG;
+  } else if (op < xp + xb && xp < op + ob) {
+    return EAAS_ERR_INVALID_ARG;
+  }
+  const WsLayout L = layout(*s);
+  if (!ws || !aligned16(ws) || ws_bytes < L.total) return EAAS_ERR_WORKSPACE;
+  char* base = static_cast<char*>(ws);
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  const eaas_routing rt = r ? *r : ws_routing(base, L);
+  auto mark = [&](int i) -> hipError_t {
+    if (!events || !events[i]) return hipSuccess;
+    return hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), hs);
+  };
+  if (mark(0) != hipSuccess) return EAAS_ERR_HIP;
+  hipError_t e = launch_route_permute(topk_ids, s->T * s->k, s->E, rt,
+                                      reinterpret_cast<int32_t*>(base + L.hist), hs);
+  if (e != hipSuccess) return EAAS_ERR_HIP;
+  float* stage = reinterpret_cast<float*>(base + L.stage);
+  FfnArgs a{};
+  a.T = s->T; a.H = s->H; a.I = s->I; a.E = s->E; a.k = s->k;
+  a.x = static_cast<const uint16_t*>(x);
+  a.perm = rt.perm;
+  a.offsets = rt.offsets;
+  a.active = rt.active;
+  a.w_gate_up = w_gate_up;
+  a.s_gate_up = w_gate_up_scale;
+  a.w_down = w_down;
+  a.s_down = w_down_scale;
+  a.fp8 = w_dtype == EAAS_FP8_E4M3;
+  a.h = reinterpret_cast<uint16_t*>(base + L.h);
+  a.y = stage;
+  a.topk_weights = topk_weights;
+  a.epilogue = kDownWeighted;
+  if (mark(1) != hipSuccess) return EAAS_ERR_HIP;
+  e = launch_gate_up(a, hs);
+  if (e != hipSuccess || mark(2) != hipSuccess) return EAAS_ERR_HIP;
+  e = launch_down(a, hs);
+  if (e != hipSuccess || mark(3) != hipSuccess) return EAAS_ERR_HIP;
+  e = launch_combine(stage, rt.inv, topk_weights, s->T, s->H, s->k, true, out,
+                     out_dtype == EAAS_FP32, hs);
+  if (e != hipSuccess || mark(4) != hipSuccess) return EAAS_ERR_HIP;
+  return EAAS_OK;
+}
+
+int eaas_expert_forward(const eaas_shape* s, const void* x, const int32_t* topk_ids,
+                        const float* topk_weights, const void* w_gate_up,
+                        const float* w_gate_up_scale, const void* w_down,
+                        const float* w_down_scale, int w_dtype, void* out, int out_dtype,
+                        const eaas_routing* r, void* ws, size_t ws_bytes, void* stream) {
+  return eaas_expert_forward_profiled(s, x, topk_ids, topk_weights, w_gate_up, w_gate_up_scale,
+                                      w_down, w_down_scale, w_dtype, out, out_dtype, r, ws,
+                                      ws_bytes, stream, nullptr);
+}
+
+const char* eaas_status_string(int status) {
+  switch (status) {
+    case EAAS_OK: return "ok";
+    case EAAS_ERR_INVALID_ARG: return "invalid argument";
+    case EAAS_ERR_UNSUPPORTED: return "unsupported shape";
+    case EAAS_ERR_WORKSPACE: return "workspace missing or too small";
+    case EAAS_ERR_HIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,55 @@
+// Host-side launchers shared between the C ABI and the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/eaas.h"
+
+namespace eaas {
+
+// Slots handled by one workgroup of the histogram and scatter kernels.
+constexpr int kRouteChunk = 2048;
+
+inline int route_blocks(int R) { return (R + kRouteChunk - 1) / kRouteChunk; }
+
+// Enqueue the three routing kernels.  `hist` holds route_blocks(R) * E ints.
+hipError_t launch_route_permute(const int32_t* ids, int R, int E,
+                                const eaas_routing& r, int32_t* hist,
+                                hipStream_t stream);
+
+// Which epilogue the down projection uses.
+enum DownEpilogue {
+  kDownPlain = 0,     // y[r, :] = Y[r, :] (rows in permuted order)
+  kDownWeighted = 1,  // y[perm[r], :] = w[perm[r]] * Y[r, :] (rows by slot)
+};
+
+struct FfnArgs {
+  int T, H, I, E, k;
+  const uint16_t* x;          // [T,H] bf16
+  const int32_t* perm;        // [R]
+  const int32_t* offsets;     // [E+1]
+  const int32_t* active;      // [E+1]
+  const void* w_gate_up;      // [E,2I,H]
+  const float* s_gate_up;     // [E,2I/128,H/128] (fp8 only)
+  const void* w_down;         // [E,H,I]
+  const float* s_down;        // [E,H/128,I/128] (fp8 only)
+  bool fp8;
+  uint16_t* h;                // [R,I] bf16 scratch
+  float* y;                   // [R,H] fp32
+  const float* topk_weights;  // [R] (weighted epilogue)
+  int epilogue;               // DownEpilogue
+};
+
+// Gate/up GEMM with the SiLU*mul epilogue into h.
+hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream);
+// Down GEMM from h into y (epilogue per a.epilogue).
+hipError_t launch_down(const FfnArgs& a, hipStream_t stream);
+
+// out[t] = sum_j (weighted ? y[s] : w[s] * y[inv[s]]) over valid slots s = t*k+j.
+hipError_t launch_combine(const float* y, const int32_t* inv, const float* w,
+                          int T, int H, int k, bool rows_by_slot_weighted,
+                          void* out, bool out_fp32, hipStream_t stream);
+
+}  // namespace eaas

@@ -1,0 +1,209 @@
+"""Python binding of libeaas.so: argument marshalling for the C ABI in
+include/eaas.h, nothing else.  Every step of the forward pass runs in the HIP
+kernels of the library; torch tensors are used only as device buffers and
+torch streams as HIP streams.  There is no CPU fallback: if the library is not
+built, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+from pathlib import Path
+
+import torch
+
+__all__ = [
+    "EAAS_OK", "EAAS_BF16", "EAAS_FP8_E4M3", "EAAS_FP32", "EaasError", "lib",
+    "library_path", "eaas_workspace_bytes", "eaas_route_permute",
+    "eaas_expert_ffn_grouped", "eaas_unpermute_combine", "eaas_expert_forward",
+    "eaas_status_string", "eaas_expert_forward_profiled", "alloc_routing",
+    "alloc_workspace", "EXPORTED",
+]
+
+EAAS_OK = 0
+EAAS_BF16, EAAS_FP8_E4M3, EAAS_FP32 = 0, 1, 2
+EXPORTED = ("eaas_workspace_bytes", "eaas_route_permute", "eaas_expert_ffn_grouped",
+            "eaas_unpermute_combine", "eaas_expert_forward", "eaas_expert_forward_profiled",
+            "eaas_status_string")
+
+_LIB_PATH = Path(__file__).resolve().parent / "libeaas.so"
+_lib = None
+
+
+class EaasError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {eaas_status_string(status)} (status {status})")
+        self.status = status
+
+
+class _Shape(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("H", ctypes.c_int32), ("I", ctypes.c_int32),
+                ("E", ctypes.c_int32), ("k", ctypes.c_int32)]
+
+
+class _Routing(ctypes.Structure):
+    _fields_ = [("counts", ctypes.c_void_p), ("offsets", ctypes.c_void_p),
+                ("perm", ctypes.c_void_p), ("inv", ctypes.c_void_p),
+                ("active", ctypes.c_void_p)]
+
+
+def library_path() -> Path:
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    """Load libeaas.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not _LIB_PATH.exists():
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(str(_LIB_PATH))
+        vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+        sp, rp = ctypes.POINTER(_Shape), ctypes.POINTER(_Routing)
+        L.eaas_workspace_bytes.argtypes = [sp, i32]
+        L.eaas_workspace_bytes.restype = sz
+        L.eaas_route_permute.argtypes = [sp, vp, rp, vp, sz, vp]
+        L.eaas_route_permute.restype = i32
+        L.eaas_expert_ffn_grouped.argtypes = [sp, vp, rp, vp, vp, vp, vp, i32, vp, vp, sz, vp]
+        L.eaas_expert_ffn_grouped.restype = i32
+        L.eaas_unpermute_combine.argtypes = [sp, vp, rp, vp, vp, i32, vp]
+        L.eaas_unpermute_combine.restype = i32
+        L.eaas_expert_forward.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, rp, vp, sz, vp]
+        L.eaas_expert_forward.restype = i32
+        L.eaas_expert_forward_profiled.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32,
+                                                   rp, vp, sz, vp, vp]
+        L.eaas_expert_forward_profiled.restype = i32
+        L.eaas_status_string.argtypes = [i32]
+        L.eaas_status_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def eaas_status_string(status: int) -> str:
+    return lib().eaas_status_string(int(status)).decode()
+
+
+def _shape(T, H, I, E, k) -> _Shape:
+    return _Shape(int(T), int(H), int(I), int(E), int(k))
+
+
+def _p(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_contiguous():
+        raise ValueError("tensor arguments must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _routing(r) -> _Routing | None:
+    if r is None:
+        return None
+    return _Routing(_p(r["counts"]), _p(r["offsets"]), _p(r["perm"]), _p(r["inv"]), _p(r["active"]))
+
+
+def _check(status: int, where: str) -> None:
+    if status != EAAS_OK:
+        raise EaasError(status, where)
+
+
+def _wdtype(w: torch.Tensor) -> int:
+    if w.element_size() == 1:
+        return EAAS_FP8_E4M3
+    if w.element_size() == 2:
+        return EAAS_BF16
+    raise ValueError("weights must be bf16 (2-byte) or fp8-e4m3 (1-byte) tensors")
+
+
+def eaas_workspace_bytes(T, H, I, E, k, w_dtype=EAAS_BF16) -> int:
+    s = _shape(T, H, I, E, k)
+    return int(lib().eaas_workspace_bytes(ctypes.byref(s), int(w_dtype)))
+
+
+def alloc_workspace(T, H, I, E, k, w_dtype=EAAS_BF16, device="cuda") -> torch.Tensor:
+    n = eaas_workspace_bytes(T, H, I, E, k, w_dtype)
+    if n == 0:
+        raise EaasError(-2, "eaas_workspace_bytes")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def alloc_routing(T, k, E, device="cuda") -> dict:
+    R = T * k
+    z = lambda n: torch.empty(max(n, 1), dtype=torch.int32, device=device)  # noqa: E731
+    return dict(counts=z(E), offsets=z(E + 1), perm=z(R), inv=z(R), active=z(E + 1))
+
+
+def eaas_route_permute(topk_ids: torch.Tensor, E: int, routing: dict, ws: torch.Tensor,
+                       H: int = 128, I: int = 128, stream=None) -> None:
+    T, k = topk_ids.shape
+    s = _shape(T, H, I, E, k)
+    r = _routing(routing)
+    st = lib().eaas_route_permute(ctypes.byref(s), _p(topk_ids), ctypes.byref(r), _p(ws),
+                                  ws.numel(), _stream(stream))
+    _check(st, "eaas_route_permute")
+
+
+def eaas_expert_ffn_grouped(x: torch.Tensor, routing: dict, w_gate_up: torch.Tensor,
+                            w_down: torch.Tensor, y_perm: torch.Tensor, ws: torch.Tensor,
+                            k: int, w_gate_up_scale=None, w_down_scale=None, stream=None) -> None:
+    T, H = x.shape
+    E, twoI, _ = w_gate_up.shape
+    s = _shape(T, H, twoI // 2, E, k)
+    r = _routing(routing)
+    st = lib().eaas_expert_ffn_grouped(
+        ctypes.byref(s), _p(x), ctypes.byref(r), _p(w_gate_up), _p(w_gate_up_scale),
+        _p(w_down), _p(w_down_scale), _wdtype(w_gate_up), _p(y_perm), _p(ws), ws.numel(),
+        _stream(stream))
+    _check(st, "eaas_expert_ffn_grouped")
+
+
+def eaas_unpermute_combine(y_perm: torch.Tensor, routing: dict, topk_weights: torch.Tensor,
+                           out: torch.Tensor, E: int, I: int = 128, stream=None) -> None:
+    T, k = topk_weights.shape
+    H = out.shape[1]
+    s = _shape(T, H, I, E, k)
+    r = _routing(routing)
+    odt = EAAS_FP32 if out.dtype == torch.float32 else EAAS_BF16
+    st = lib().eaas_unpermute_combine(ctypes.byref(s), _p(y_perm), ctypes.byref(r),
+                                      _p(topk_weights), _p(out), odt, _stream(stream))
+    _check(st, "eaas_unpermute_combine")
+
+
+def eaas_expert_forward(x: torch.Tensor, topk_ids: torch.Tensor, topk_weights: torch.Tensor,
+                        w_gate_up: torch.Tensor, w_down: torch.Tensor, out: torch.Tensor,
+                        ws: torch.Tensor, w_gate_up_scale=None, w_down_scale=None,
+                        routing: dict | None = None, stream=None, events=None) -> None:
+    """events: optional 5 torch.cuda.Event(enable_timing=True) recorded on the
+    stream around routing, gate/up, down and combine (profiled entry point)."""
+    T, H = x.shape
+    E, twoI, _ = w_gate_up.shape
+    k = topk_ids.shape[1]
+    s = _shape(T, H, twoI // 2, E, k)
+    r = _routing(routing)
+    odt = EAAS_FP32 if out.dtype == torch.float32 else EAAS_BF16
+    args = (ctypes.byref(s), _p(x), _p(topk_ids), _p(topk_weights), _p(w_gate_up),
+            _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up), _p(out), odt,
+            ctypes.byref(r) if r is not None else None, _p(ws), ws.numel(), _stream(stream))
+    if events is None:
+        _check(lib().eaas_expert_forward(*args), "eaas_expert_forward")
+        return
+    if len(events) != 5:
+        raise ValueError("events must hold 5 entries")
+    ev = (ctypes.c_void_p * 5)(*[e.cuda_event if e is not None else None for e in events])
+    _check(lib().eaas_expert_forward_profiled(*args, ev), "eaas_expert_forward_profiled")
+
+
+def eaas_expert_forward_profiled(*args, events, **kwargs) -> None:
+    """eaas_expert_forward with timing events (see eaas_expert_forward)."""
+    for e in events:
+        if e is not None and not e.cuda_event:
+            e.record()  # torch creates the underlying HIP event lazily
+    eaas_expert_forward(*args, events=events, **kwargs)

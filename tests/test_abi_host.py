@@ -1,0 +1,124 @@
+"""C ABI host side, no GPU: the library loads, exports every declared symbol,
+and rejects bad arguments on the host before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2509_17863_amd import eaas
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "eaas.h")).read()
+    return sorted(set(re.findall(r"\b(eaas_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_exported_set():
+    assert _declared() == sorted(eaas.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    L = eaas.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+
+
+def test_status_strings():
+    assert eaas.eaas_status_string(0) == "ok"
+    assert "workspace" in eaas.eaas_status_string(-3)
+
+
+def shape(T=64, H=256, I=128, E=8, k=2):
+    return eaas._Shape(T, H, I, E, k)
+
+
+@pytest.mark.parametrize("kw,ok", [
+    (dict(), True), (dict(T=0), True), (dict(H=200), False), (dict(I=100), False),
+    (dict(E=0), False), (dict(E=1025), False), (dict(k=0), False), (dict(k=65), False),
+    (dict(T=-1), False), (dict(T=1 << 28, k=8), False),
+])
+def test_workspace_bytes_validation(kw, ok):
+    s = shape(**kw)
+    n = eaas.lib().eaas_workspace_bytes(ctypes.byref(s), 0)
+    assert (n > 0) == ok
+    if ok:
+        assert n % 256 == 0
+        assert eaas.lib().eaas_workspace_bytes(ctypes.byref(s), 7) == 0
+
+
+def test_workspace_covers_stage_and_h():
+    T, H, I, E, k = 100, 512, 256, 8, 4
+    n = eaas.eaas_workspace_bytes(T, H, I, E, k)
+    assert n >= T * k * H * 4 + T * k * I * 2
+
+
+FAKE = 1 << 20  # host-only: these calls must be rejected before any device work
+
+
+def _routing(p=FAKE):
+    return eaas._Routing(p, p, p, p, p)
+
+
+def test_route_permute_rejects_bad_args():
+    L = eaas.lib()
+    s = shape()
+    r = _routing()
+    assert L.eaas_route_permute(None, FAKE, ctypes.byref(r), FAKE, 1 << 30, None) == -1
+    assert L.eaas_route_permute(ctypes.byref(s), None, ctypes.byref(r), FAKE, 1 << 30, None) == -1
+    assert L.eaas_route_permute(ctypes.byref(s), FAKE, None, FAKE, 1 << 30, None) == -1
+    assert L.eaas_route_permute(ctypes.byref(s), FAKE, ctypes.byref(r), None, 1 << 30, None) == -3
+    assert L.eaas_route_permute(ctypes.byref(s), FAKE, ctypes.byref(r), FAKE, 16, None) == -3
+    bad = shape(H=96)
+    assert L.eaas_route_permute(ctypes.byref(bad), FAKE, ctypes.byref(r), FAKE, 1 << 30, None) == -2
+    empty = shape(T=0)
+    assert L.eaas_route_permute(ctypes.byref(empty), None, None, None, 0, None) == 0
+
+
+def test_forward_rejects_bad_args():
+    L = eaas.lib()
+    s = shape()
+    big = 1 << 34
+
+    def fwd(x=FAKE, ids=FAKE, w=FAKE, wgu=FAKE, sgu=None, wd=FAKE, sd=None, wdt=0, out=FAKE * 64,
+            odt=0, r=None, ws=FAKE, wsb=big, sh=s):
+        return L.eaas_expert_forward(ctypes.byref(sh) if sh is not None else None, x, ids, w,
+                                     wgu, sgu, wd, sd, wdt, out, odt, r, ws, wsb, None)
+
+    assert fwd(sh=None) == -1
+    assert fwd(x=None) == -1
+    assert fwd(ids=None) == -1
+    assert fwd(wgu=None) == -1
+    assert fwd(wdt=1) == -1            # fp8 without scales
+    assert fwd(wdt=5) == -1            # unknown weight dtype
+    assert fwd(odt=1) == -1            # fp8 output is not offered
+    assert fwd(x=FAKE + 8) == -1       # misaligned
+    assert fwd(out=FAKE + 256) == -1   # partial overlap with x
+    assert fwd(out=FAKE, odt=2) == -1  # fp32 output cannot alias bf16 x
+    assert fwd(ws=None) == -3
+    assert fwd(wsb=1024) == -3
+    assert fwd(sh=shape(E=2000)) == -2
+    assert fwd(sh=shape(T=0), x=None, ids=None) == 0
+
+
+def test_ffn_and_combine_reject_bad_args():
+    L = eaas.lib()
+    s = shape()
+    r = _routing()
+    assert L.eaas_expert_ffn_grouped(ctypes.byref(s), FAKE, ctypes.byref(r), FAKE, None, FAKE,
+                                     None, 1, FAKE, FAKE, 1 << 34, None) == -1
+    assert L.eaas_expert_ffn_grouped(ctypes.byref(s), FAKE, ctypes.byref(r), FAKE, None, FAKE,
+                                     None, 0, None, FAKE, 1 << 34, None) == -1
+    assert L.eaas_unpermute_combine(ctypes.byref(s), FAKE, ctypes.byref(r), FAKE, FAKE, 1,
+                                    None) == -1
+    assert L.eaas_unpermute_combine(ctypes.byref(s), FAKE, ctypes.byref(r), None, FAKE, 0,
+                                    None) == -1
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(eaas, "_LIB_PATH", tmp_path / "libeaas.so")
+    monkeypatch.setattr(eaas, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        eaas.lib()
