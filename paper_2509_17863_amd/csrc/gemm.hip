@@ -1,25 +1,31 @@
 // Grouped expert GEMMs over the reorganised token rows (EaaS §3.3 "grouped
 // GEMM"; scheduler over the compacted active-expert list of §4.1).
 //
-// One kernel template serves both projections of the SwiGLU expert:
+// Both projections of the SwiGLU expert use the same machinery:
 //   gate/up:  C[r, n] = x[perm[r]/k, :] . W_gate_up[e][n, :]   (rows gathered)
 //             epilogue h[r, c] = bf16(silu(C_gate[r, c]) * C_up[r, c])
 //   down:     C[r, n] = h[r, :] . W_down[e][n, :]
 //             epilogue y[perm[r], n] = w[perm[r]] * C (fp32, rows by slot) or
 //                      y[r, n] = C (fp32, rows in permuted order)
 //
-// Tiles: BM token rows x BN weight rows, BK = 64 along the reduction.  Each of
-// the WM x WN waves owns MBW x NBW blocks of 32x32 computed with
-// v_mfma_f32_32x32x16_bf16 (src0 = weight rows, src1 = token rows, so a lane
-// ends up holding 4 consecutive output columns of one token row).  Operand
-// tiles go global -> registers -> LDS (double buffered; the next tile's loads
-// are in flight during the current tile's MFMAs).  LDS rows are 128 bytes
-// (64 bf16); 16-byte chunk c of row r sits at chunk c ^ (r & 7), so the
-// 32-row fragment reads and the row-wise writes are bank-conflict free.
+// A tile is BM token rows x BN weight rows.  Each of the WM x WN waves owns
+// MBW x NBW blocks of 32x32 computed with v_mfma_f32_32x32x16_bf16 (src0 =
+// weight rows, src1 = token rows, so a lane ends up holding 4 consecutive
+// output columns of one token row).  For gate/up the BN weight rows are BN/2
+// gate rows followed by the matching BN/2 up rows, and each wave's blocks pair
+// a gate block with the up block of the same columns.
 //
-// fp8-e4m3 weights (one fp32 scale per 128x128 block) are converted to bf16
-// exactly when written to LDS; the MFMA partial sum of every 128-wide K block
-// is multiplied by its block scale and added to the fp32 accumulator.
+// Two main loops:
+//   * bf16 weights: operands go global -> LDS directly (global_load_lds, 16 B
+//     per lane, no VGPR staging) through a ring of STAGES buffers; tile kt+S-1
+//     is in flight while tile kt is multiplied.  Waits are explicit vmcnt
+//     counts plus a bare s_barrier.
+//   * fp8-e4m3 weights (one fp32 scale per 128x128 block): operands go global
+//     -> VGPR -> LDS (double buffered) so the weights can be converted to bf16
+//     on the way (exact); each 128-wide K block's MFMA partial sum is scaled
+//     and added to the fp32 accumulator.
+// LDS rows are BK bf16 long; 16-byte chunk c of row r is stored at chunk
+// c ^ swz(r) so 32-row fragment reads hit every bank once.
 //
 // Scheduling: the workgroup reads the compacted active list (group-shrink)
 // into LDS once and builds the per-expert M-tile prefix there.  Tile ids are
@@ -34,7 +40,8 @@
 namespace eaas {
 namespace {
 
-constexpr int kBK = 64;
+#define LDS_AS __attribute__((address_space(3)))
+
 constexpr int kNumXcd = 8;
 
 enum GemmKind { kGateUp = 0, kDownPlainK = 1, kDownWeightedK = 2 };
@@ -58,9 +65,400 @@ struct GemmParams {
   int E;                  // resident experts
 };
 
+struct Tile {
+  int e;           // expert
+  int tn;          // weight (N) tile
+  int r0;          // first permuted row of the tile
+  int rows_valid;  // rows of the tile that belong to the expert
+};
+
 __device__ __forceinline__ float silu_mul(float g, float u) {
   return g / (1.0f + __expf(-g)) * u;
 }
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// One wave-wide 16-byte-per-lane DMA from global memory into LDS: lane l
+// reads 16 bytes at base + voff(l) and they land at LDS byte address
+// lds + 16*l.  Issued from inline assembly so the compiler adds no waits of
+// its own; completion is tracked with explicit vmcnt waits.  `base` and `lds`
+// are wave-uniform (SGPRs; `lds` goes to M0).
+__device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(voff), "s"(base), "s"(lds) : "memory");
+}
+
+// Group-shrink schedule: the active list and its M-tile prefix go to LDS once,
+// then this workgroup's tile is located.  Returns false for surplus groups.
+template <int BM, int BN, int NT>
+__device__ __forceinline__ bool locate_tile(const GemmParams& p, int* s_tp, int* s_exp,
+                                            int* s_wave, Tile& t) {
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  // routing arrays may come from the caller: clamp every index taken from them
+  const int n_active = min(max(p.active[0], 0), p.E);
+  constexpr int PER = (kMaxExperts + NT) / NT;  // entries per thread (plus the end)
+  int loc[PER];
+  int sum = 0;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int a = tid * PER + i;
+    int c = 0;
+    if (a < n_active) {
+      const int e = min(max(p.active[1 + a], 0), p.E - 1);
+      s_exp[a] = e;
+      const int beg = min(max(p.offsets[e], 0), p.R);
+      const int end = min(max(p.offsets[e + 1], beg), p.R);
+      c = ceil_div(end - beg, BM);
+    }
+    loc[i] = c;
+    sum += c;
+  }
+  int incl = sum;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int o = __shfl_up(incl, d, kWave);
+    if (lane >= d) incl += o;
+  }
+  if (lane == kWave - 1) s_wave[wave] = incl;
+  __syncthreads();
+  int before = 0;
+#pragma unroll
+  for (int w = 0; w < NT / kWave; ++w) before += (w < wave) ? s_wave[w] : 0;
+  int run = before + incl - sum;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int a = tid * PER + i;
+    if (a <= n_active) s_tp[a] = run;
+    run += loc[i];
+  }
+  __syncthreads();
+  const int n_tiles_n = p.N / BN;
+  const int total = s_tp[n_active] * n_tiles_n;
+  const int bid = blockIdx.x;
+  if (bid >= total) return false;
+  int tile = bid;
+  const int per = total / kNumXcd;
+  if (bid < per * kNumXcd) tile = (bid % kNumXcd) * per + bid / kNumXcd;
+  int lo = 0, hi = n_active - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (s_tp[mid] * n_tiles_n <= tile) lo = mid; else hi = mid - 1;
+  }
+  const int e = s_exp[lo];
+  const int mt = s_tp[lo + 1] - s_tp[lo];
+  const int local = tile - s_tp[lo] * n_tiles_n;
+  t.e = e;
+  t.tn = local / mt;
+  const int tm = local - t.tn * mt;
+  const int beg = min(max(p.offsets[e], 0), p.R);
+  const int end = min(max(p.offsets[e + 1], beg), p.R);
+  t.r0 = beg + tm * BM;
+  t.rows_valid = min(BM, end - t.r0);
+  return true;
+}
+
+// Weight row (of the expert's [N, K] matrix) held by LDS row j of an N tile.
+template <bool GATEUP, int BN>
+__device__ __forceinline__ int weight_row(const GemmParams& p, int tn, int j) {
+  if (GATEUP) return j < BN / 2 ? tn * (BN / 2) + j : p.I + tn * (BN / 2) + (j - BN / 2);
+  return tn * BN + j;
+}
+
+// First LDS weight row of N block j of wave column wn.
+template <bool GATEUP, int BN, int NBW>
+__device__ __forceinline__ int block_row(int wn, int j) {
+  if (GATEUP) {
+    constexpr int HB = NBW / 2;
+    return j < HB ? wn * HB * 32 + j * 32 : BN / 2 + wn * HB * 32 + (j - HB) * 32;
+  }
+  return wn * NBW * 32 + j * 32;
+}
+
+// acc[i][j][v]: token row am0 + i*32 + lane%32, weight row
+// block_row(j) + 8*(v/4) + 4*(lane/32) + v%4.
+template <int KIND, int BN, int MBW, int NBW>
+__device__ __forceinline__ void epilogue(const GemmParams& p, const Tile& t, int wn, int am0,
+                                         int mb_live, const f32x16 (&acc)[MBW][NBW]) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int lrow = lane & 31;
+  const int khalf = lane >> 5;
+#pragma unroll
+  for (int i = 0; i < MBW; ++i) {
+    const int rr = am0 + i * 32 + lrow;
+    if (i >= mb_live || rr >= t.rows_valid) continue;
+    const int r = t.r0 + rr;
+    if (KIND == kGateUp) {
+      constexpr int HB = NBW / 2;
+      uint16_t* hrow = p.h + (size_t)r * p.I + t.tn * (BN / 2) + wn * HB * 32;
+#pragma unroll
+      for (int j = 0; j < HB; ++j) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = j * 32 + 8 * q + 4 * khalf;
+          const f32x16 g = acc[i][j];
+          const f32x16 u = acc[i][j + HB];
+          u32x2 v;
+          v[0] = pack_bf16x2(silu_mul(g[4 * q + 0], u[4 * q + 0]), silu_mul(g[4 * q + 1], u[4 * q + 1]));
+          v[1] = pack_bf16x2(silu_mul(g[4 * q + 2], u[4 * q + 2]), silu_mul(g[4 * q + 3], u[4 * q + 3]));
+          *reinterpret_cast<u32x2*>(hrow + c) = v;
+        }
+      }
+    } else {
+      int orow = r;
+      float wt = 1.0f;
+      if (KIND == kDownWeightedK) {
+        orow = min(max(p.perm[r], 0), p.R - 1);
+        wt = p.w[orow];
+      }
+      float* yrow = p.y + (size_t)orow * p.N + t.tn * BN + wn * NBW * 32;
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = j * 32 + 8 * q + 4 * khalf;
+          f32x4 v;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const float a = acc[i][j][4 * q + u];
+            v[u] = KIND == kDownWeightedK ? wt * a : a;  // rounded product, stored
+          }
+          *reinterpret_cast<f32x4*>(yrow + c) = v;
+        }
+      }
+    }
+  }
+}
+
+// ============================================================================
+// bf16 weights: LDS-DMA ring
+// ============================================================================
+// XOR swizzle of the 16-byte chunks of an LDS row.  A fragment read has 8
+// lanes (128-byte bank lines) or 16 lanes (256-byte bank lines) in flight per
+// cycle, reading one chunk column of consecutive rows; the swizzle puts those
+// rows' chunks on distinct banks in both cases.
+template <int BK>
+__device__ __forceinline__ int swz(int row) {
+  if (BK == 64) return (row & 7) ^ ((row >> 3) & 1);      // 128-byte rows, 8 chunks
+  return ((row >> 1) & 3) ^ ((row >> 3) & 1);              // 64-byte rows, 4 chunks
+}
+
+// Global sources of a tile's DMA (shared by the full- and partial-tile loops).
+template <int A_INST, int B_INST>
+struct DmaSrc {
+  const char* a;             // A base (bytes); K tile kt starts kt*BK*2 bytes further
+  const char* b;             // B base of the expert (bytes)
+  uint32_t a_off[A_INST];    // per-lane byte offsets of this lane's DMA rows
+  uint32_t b_off[B_INST];
+  uint32_t lds;              // LDS byte address of stage 0
+  int wave;
+};
+
+template <int KIND, int BK, int STAGES, int BM, int BN, int MBW, int NBW, bool FULL>
+struct DmaLoop {
+  static constexpr int RB = BK * 2;          // bytes per LDS row
+  static constexpr int CH = RB / 16;         // 16-byte chunks per row
+  static constexpr int RPI = kWave / CH;     // rows per wave DMA instruction (1 KiB)
+  static constexpr int A_INST = BM / (4 * RPI);
+  static constexpr int B_INST = BN / (4 * RPI);
+  static constexpr int INST = A_INST + B_INST;
+  static constexpr int A_BYTES = BM * RB;
+  static constexpr int STAGE_BYTES = (BM + BN) * RB;
+  static constexpr int KK = BK / 16;         // MFMA k-steps per tile
+  static_assert(KK % 2 == 0, "fragment double buffering alternates sets");
+  static_assert(STAGES >= 2 && STAGES <= 4, "ring depth");
+  static_assert(INST % MBW == 0, "DMA instructions spread evenly over row blocks");
+
+  struct Frags {
+    bf16x8 a[MBW];
+    bf16x8 b[NBW];
+  };
+
+  using Src = DmaSrc<A_INST, B_INST>;
+
+  // DMA instruction q (0..INST-1) of K tile kt into the LDS stage at `dst`.
+  static __device__ __forceinline__ void issue_one(const Src& s, uint32_t dst, int kt, int q) {
+    const int k0b = kt * BK * 2;
+    if (q < A_INST)
+      dma16(s.a + k0b, s.a_off[q], dst + (s.wave * (BM / 4) + q * RPI) * RB);
+    else
+      dma16(s.b + k0b, s.b_off[q - A_INST],
+            dst + A_BYTES + (s.wave * (BN / 4) + (q - A_INST) * RPI) * RB);
+  }
+
+  static __device__ __forceinline__ void issue(const Src& s, uint32_t dst, int kt) {
+#pragma unroll
+    for (int q = 0; q < INST; ++q) issue_one(s, dst, kt, q);
+  }
+
+  static __device__ __forceinline__ void load_b(const LDS_AS char* src, int coff,
+                                                const int (&b_lane_off)[NBW], Frags& f) {
+#pragma unroll
+    for (int j = 0; j < NBW; ++j)
+      f.b[j] = *reinterpret_cast<const LDS_AS bf16x8*>(src + A_BYTES + b_lane_off[j] + coff);
+  }
+
+  static __device__ __forceinline__ void load_a(const LDS_AS char* src, int coff, int i,
+                                                int a_lane_off, int mb_live, Frags& f) {
+    if (FULL || i < mb_live)
+      f.a[i] = *reinterpret_cast<const LDS_AS bf16x8*>(src + a_lane_off + i * 32 * RB + coff);
+  }
+
+  static __device__ __forceinline__ void mma_row(const Frags& f, int i, int mb_live,
+                                                 f32x16 (&acc)[MBW][NBW]) {
+    if (FULL || i < mb_live)
+#pragma unroll
+      for (int j = 0; j < NBW; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
+  }
+
+  // wait until this wave's DMA of a tile has landed, `later` tiles (issued
+  // after it) possibly still in flight
+  static __device__ __forceinline__ void wait_tiles(int later) {
+    if (STAGES > 3 && later >= 2) wait_vmcnt<(STAGES > 3 ? 2 * INST : 0)>();
+    else if (STAGES > 2 && later >= 1) wait_vmcnt<(STAGES > 2 ? INST : 0)>();
+    else wait_vmcnt<0>();
+  }
+
+  // Software pipeline over K tiles (tile kt lives in stage kt % STAGES):
+  //   k-step 0 of tile kt: its MFMAs interleaved with the DMA of tile
+  //     kt+STAGES-1 (into the stage tile kt-1 used, released by the previous
+  //     barrier) and the fragment reads of the next k-step;
+  //   last k-step: half the MFMAs, then the tile boundary (wait for tile
+  //     kt+1, barrier, first fragments of tile kt+1), then the other half.
+  // The barrier also certifies that every wave finished reading tile kt, so
+  // its stage may be refilled during tile kt+1.
+  static __device__ __forceinline__ void run(const LDS_AS char* smem, const Src& s, int nk,
+                                             int a_lane_off, const int (&b_lane_off)[NBW],
+                                             int s_l, int mb_live, f32x16 (&acc)[MBW][NBW]) {
+    const int khalf = (threadIdx.x & 63) >> 5;
+    auto coff = [&](int kk) { return (((2 * kk + khalf) ^ s_l) << 4); };
+#pragma unroll
+    for (int t = 0; t < STAGES - 1; ++t)
+      if (t < nk) issue(s, s.lds + t * STAGE_BYTES, t);
+    wait_tiles(min(STAGES - 2, nk - 1));
+    lds_barrier();
+    Frags f[2];
+    load_b(smem, coff(0), b_lane_off, f[0]);
+#pragma unroll
+    for (int i = 0; i < MBW; ++i) load_a(smem, coff(0), i, a_lane_off, mb_live, f[0]);
+
+    for (int kt = 0; kt < nk; ++kt) {
+      const LDS_AS char* src = smem + (kt % STAGES) * STAGE_BYTES;
+      const int nx = kt + STAGES - 1;
+      const bool refill = nx < nk;
+      const uint32_t dst = s.lds + (nx % STAGES) * STAGE_BYTES;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        Frags& fa = f[kk & 1];
+        Frags& fb = f[(kk + 1) & 1];
+        if (kk + 1 < KK) {
+          load_b(src, coff(kk + 1), b_lane_off, fb);
+#pragma unroll
+          for (int i = 0; i < MBW; ++i) {
+            load_a(src, coff(kk + 1), i, a_lane_off, mb_live, fb);
+            mma_row(fa, i, mb_live, acc);
+            if (kk == 0 && refill) {
+#pragma unroll
+              for (int q = i * (INST / MBW); q < (i + 1) * (INST / MBW); ++q)
+                issue_one(s, dst, nx, q);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < MBW / 2; ++i) mma_row(fa, i, mb_live, acc);
+          if (kt + 1 < nk) {
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            wait_tiles(min(STAGES - 2, nk - 2 - kt));
+            lds_barrier();
+            const LDS_AS char* nsrc = smem + ((kt + 1) % STAGES) * STAGE_BYTES;
+            load_b(nsrc, coff(0), b_lane_off, fb);
+#pragma unroll
+            for (int i = 0; i < MBW; ++i) load_a(nsrc, coff(0), i, a_lane_off, mb_live, fb);
+          }
+#pragma unroll
+          for (int i = MBW / 2; i < MBW; ++i) mma_row(fa, i, mb_live, acc);
+        }
+      }
+    }
+  }
+};
+
+template <int KIND, int BK, int STAGES>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void grouped_gemm_dma_kernel(GemmParams p) {
+  constexpr int WN = 2, MBW = 4, NBW = 4;
+  constexpr int NT = 256, BM = 256, BN = 256;
+  constexpr bool GATEUP = KIND == kGateUp;
+  using Full = DmaLoop<KIND, BK, STAGES, BM, BN, MBW, NBW, true>;
+  using Part = DmaLoop<KIND, BK, STAGES, BM, BN, MBW, NBW, false>;
+  constexpr int RB = Full::RB, CH = Full::CH, RPI = Full::RPI;
+
+  __shared__ __attribute__((aligned(1024))) char smem_raw[STAGES * Full::STAGE_BYTES];
+  __shared__ int s_tp[kMaxExperts + 1];
+  __shared__ int s_exp[kMaxExperts];
+  __shared__ int s_wave[NT / kWave + 1];
+
+  Tile t;
+  if (!locate_tile<BM, BN, NT>(p, s_tp, s_exp, s_wave, t)) return;
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  // DMA: lane writes 16 bytes at (row lane/CH, physical chunk lane%CH) of its
+  // instruction's RPI rows, so it fetches logical chunk (lane%CH) ^ swz(row)
+  const int drow = lane / CH;
+  const int dpc = lane % CH;
+  typename Full::Src src;
+  src.wave = wave;
+  src.a = reinterpret_cast<const char*>(p.a);
+  src.b = reinterpret_cast<const char*>(p.b) + (size_t)t.e * p.N * p.K * 2;
+#pragma unroll
+  for (int i = 0; i < Full::A_INST; ++i) {
+    const int row = wave * (BM / 4) + i * RPI + drow;
+    const int r = t.r0 + (row < t.rows_valid ? row : 0);
+    const int src_row = GATEUP ? min(max(p.perm[r], 0), p.R - 1) / p.k : r;
+    src.a_off[i] = (uint32_t)(src_row * p.lda + ((dpc ^ swz<BK>(row)) * 8)) * 2u;
+  }
+#pragma unroll
+  for (int i = 0; i < Full::B_INST; ++i) {
+    const int j = wave * (BN / 4) + i * RPI + drow;
+    src.b_off[i] = (uint32_t)(weight_row<GATEUP, BN>(p, t.tn, j) * p.K + ((dpc ^ swz<BK>(j)) * 8)) * 2u;
+  }
+
+  const int wm = wave / WN;
+  const int wn = wave % WN;
+  const int lrow = lane & 31;
+  const int am0 = wm * MBW * 32;
+  const int a_lane_off = (am0 + lrow) * RB;
+  int b_lane_off[NBW];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) b_lane_off[j] = (block_row<GATEUP, BN, NBW>(wn, j) + lrow) * RB;
+  const int s_l = swz<BK>(lrow);
+  const int mb_live =
+      __builtin_amdgcn_readfirstlane(max(0, min(MBW, ceil_div(t.rows_valid - am0, 32))));
+
+  f32x16 acc[MBW][NBW];
+#pragma unroll
+  for (int i = 0; i < MBW; ++i)
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) acc[i][j] = f32x16{};
+
+  const LDS_AS char* smem = (const LDS_AS char*)smem_raw;  // generic -> LDS address space
+  src.lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
+  const int nk = p.K / BK;
+  if (t.rows_valid == BM)
+    Full::run(smem, src, nk, a_lane_off, b_lane_off, s_l, mb_live, acc);
+  else
+    Part::run(smem, src, nk, a_lane_off, b_lane_off, s_l, mb_live, acc);
+
+  epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, acc);
+}
+
+// ============================================================================
+// fp8 weights (and generic shapes): register-staged double buffer, BK = 64
+// ============================================================================
+constexpr int kBK = 64;
 
 // 16 fp8-e4m3 values -> 16 bf16 (exact), as two 16-byte chunks.
 __device__ __forceinline__ void fp8x16_to_bf16(const u32x4 q, u32x4& lo, u32x4& hi) {
@@ -96,79 +494,13 @@ void grouped_gemm_kernel(GemmParams p) {
   __shared__ int s_exp[kMaxExperts];
   __shared__ int s_wave[NT / kWave + 1];
 
+  Tile t;
+  if (!locate_tile<BM, BN, NT>(p, s_tp, s_exp, s_wave, t)) return;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
+  const int e = t.e, tn = t.tn, r0 = t.r0, rows_valid = t.rows_valid;
 
-  // ---- group-shrink: active experts and their M-tile prefix, in LDS once ----
-  // routing arrays may come from the caller: clamp every index taken from them
-  const int n_active = min(max(p.active[0], 0), p.E);
-  {
-    // each thread scans PER consecutive entries of the active list (plus the end)
-    constexpr int PER = (kMaxExperts + NT) / NT;
-    int loc[PER];
-    int sum = 0;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int a = tid * PER + i;
-      int t = 0;
-      if (a < n_active) {
-        const int e = min(max(p.active[1 + a], 0), p.E - 1);
-        s_exp[a] = e;
-        const int beg = min(max(p.offsets[e], 0), p.R);
-        const int end = min(max(p.offsets[e + 1], beg), p.R);
-        t = ceil_div(end - beg, BM);
-      }
-      loc[i] = t;
-      sum += t;
-    }
-    int incl = sum;
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-      const int o = __shfl_up(incl, d, kWave);
-      if (lane >= d) incl += o;
-    }
-    if (lane == kWave - 1) s_wave[wave] = incl;
-    __syncthreads();
-    int before = 0;
-#pragma unroll
-    for (int w = 0; w < NT / kWave; ++w) before += (w < wave) ? s_wave[w] : 0;
-    int run = before + incl - sum;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int a = tid * PER + i;
-      if (a <= n_active) s_tp[a] = run;
-      run += loc[i];
-    }
-    __syncthreads();
-  }
-  const int n_tiles_n = p.N / BN;
-  const int total = s_tp[n_active] * n_tiles_n;
-  const int bid = blockIdx.x;
-  if (bid >= total) return;
-  int tile = bid;
-  {
-    const int per = total / kNumXcd;
-    if (bid < per * kNumXcd) tile = (bid % kNumXcd) * per + bid / kNumXcd;
-  }
-  // find active index a with s_tp[a]*n_tiles_n <= tile < s_tp[a+1]*n_tiles_n
-  int lo = 0, hi = n_active - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (s_tp[mid] * n_tiles_n <= tile) lo = mid; else hi = mid - 1;
-  }
-  const int a_idx = lo;
-  const int e = s_exp[a_idx];
-  const int mt = s_tp[a_idx + 1] - s_tp[a_idx];
-  const int local = tile - s_tp[a_idx] * n_tiles_n;
-  const int tn = local / mt;
-  const int tm = local - tn * mt;
-  const int row_beg = min(max(p.offsets[e], 0), p.R);
-  const int row_end = min(max(p.offsets[e + 1], row_beg), p.R);
-  const int r0 = row_beg + tm * BM;
-  const int rows_valid = min(BM, row_end - r0);
-
-  // ---- operand sources ----
   // A: thread loads chunk (tid % 8) of rows tid/8 + i*ROWS_PER_PASS
   const int a_chunk = tid & 7;
   int a_off[A_LOADS];
@@ -179,7 +511,6 @@ void grouped_gemm_kernel(GemmParams p) {
     const int src_row = GATEUP ? min(max(p.perm[r], 0), p.R - 1) / p.k : r;
     a_off[i] = src_row * p.lda + a_chunk * 8;
   }
-  // B: weight rows of this tile (gate/up: BN/2 gate rows then the matching up rows)
   const size_t esz = FP8 ? 1 : 2;
   const uint8_t* bexp = p.b + (size_t)e * p.N * p.K * esz;
   constexpr int B_CHUNKS = FP8 ? 4 : 8;  // 16-byte chunks per 64-wide K slice
@@ -188,9 +519,7 @@ void grouped_gemm_kernel(GemmParams p) {
 #pragma unroll
   for (int i = 0; i < B_LOADS; ++i) {
     const int j = tid / B_CHUNKS + i * B_ROWS_PER_PASS;
-    int wrow;
-    if (GATEUP) wrow = j < BN / 2 ? tn * (BN / 2) + j : p.I + tn * (BN / 2) + (j - BN / 2);
-    else wrow = tn * BN + j;
+    const int wrow = weight_row<GATEUP, BN>(p, tn, j);
     b_off[i] = (wrow * p.K + b_chunk * 16 / (int)esz) * (int)esz;  // bytes
   }
 
@@ -225,24 +554,16 @@ void grouped_gemm_kernel(GemmParams p) {
     }
   };
 
-  // ---- wave tile ----
   const int wm = wave / WN;
   const int wn = wave % WN;
   const int lrow = lane & 31;
   const int khalf = lane >> 5;
   const int am0 = wm * MBW * 32;  // first token row of this wave inside the tile
-  int bn0[NBW];                   // first LDS weight row of each N block
+  int bn0[NBW];
 #pragma unroll
-  for (int j = 0; j < NBW; ++j) {
-    if (GATEUP) {
-      constexpr int HB = NBW / 2;
-      bn0[j] = j < HB ? wn * HB * 32 + j * 32 : BN / 2 + wn * HB * 32 + (j - HB) * 32;
-    } else {
-      bn0[j] = wn * NBW * 32 + j * 32;
-    }
-  }
-  // number of 32-row blocks of this wave that hold valid rows (uniform)
-  const int mb_live = max(0, min(MBW, ceil_div(rows_valid - am0, 32)));
+  for (int j = 0; j < NBW; ++j) bn0[j] = block_row<GATEUP, BN, NBW>(wn, j);
+  const int mb_live =
+      __builtin_amdgcn_readfirstlane(max(0, min(MBW, ceil_div(rows_valid - am0, 32))));
 
   f32x16 acc[MBW][NBW];
   f32x16 part[FP8 ? MBW : 1][FP8 ? NBW : 1];
@@ -295,10 +616,7 @@ void grouped_gemm_kernel(GemmParams p) {
       const float* sexp = p.b_scale + (size_t)e * (p.N / 128) * (p.K / 128);
 #pragma unroll
       for (int j = 0; j < NBW; ++j) {
-        const int lr = bn0[j];
-        int wrow;
-        if (GATEUP) wrow = lr < BN / 2 ? tn * (BN / 2) + lr : p.I + tn * (BN / 2) + (lr - BN / 2);
-        else wrow = tn * BN + lr;
+        const int wrow = weight_row<GATEUP, BN>(p, tn, bn0[j]);
         const float sc = sexp[(wrow / 128) * (p.K / 128) + kb];
 #pragma unroll
         for (int i = 0; i < MBW; ++i) {
@@ -310,67 +628,34 @@ void grouped_gemm_kernel(GemmParams p) {
     if (kt + 1 < nk) store_lds(cur ^ 1);
     __syncthreads();
   }
+  epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, acc);
+}
 
-  // ---- epilogue ----
-  // acc[i][j][v]: token row am0 + i*32 + lrow, weight row bn0[j] + 8*(v/4) + 4*khalf + v%4
-#pragma unroll
-  for (int i = 0; i < MBW; ++i) {
-    const int rr = am0 + i * 32 + lrow;
-    if (i >= mb_live || rr >= rows_valid) continue;
-    const int r = r0 + rr;
-    if (GATEUP) {
-      constexpr int HB = NBW / 2;
-      uint16_t* hrow = p.h + (size_t)r * p.I + tn * (BN / 2) + wn * HB * 32;
-#pragma unroll
-      for (int j = 0; j < HB; ++j) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int c = j * 32 + 8 * q + 4 * khalf;
-          const f32x16 g = acc[i][j];
-          const f32x16 u = acc[i][j + HB];
-          u32x2 v;
-          v[0] = pack_bf16x2(silu_mul(g[4 * q + 0], u[4 * q + 0]), silu_mul(g[4 * q + 1], u[4 * q + 1]));
-          v[1] = pack_bf16x2(silu_mul(g[4 * q + 2], u[4 * q + 2]), silu_mul(g[4 * q + 3], u[4 * q + 3]));
-          *reinterpret_cast<u32x2*>(hrow + c) = v;
-        }
-      }
-    } else {
-      int orow = r;
-      float wt = 1.0f;
-      if (KIND == kDownWeightedK) {
-        orow = min(max(p.perm[r], 0), p.R - 1);
-        wt = p.w[orow];
-      }
-      float* yrow = p.y + (size_t)orow * p.N + tn * BN + wn * NBW * 32;
-#pragma unroll
-      for (int j = 0; j < NBW; ++j) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int c = j * 32 + 8 * q + 4 * khalf;
-          f32x4 v;
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            const float a = acc[i][j][4 * q + t];
-            v[t] = KIND == kDownWeightedK ? wt * a : a;  // rounded product, stored
-          }
-          *reinterpret_cast<f32x4*>(yrow + c) = v;
-        }
-      }
-    }
-  }
+// worst case M-tiles over any routing of R rows onto at most min(E, R) experts
+inline long long grid_tiles(int R, int E, int BM, int BN, int N) {
+  const long long mt = (long long)(R + BM - 1) / BM + (E < R ? E : R);
+  return mt * (N / BN);
 }
 
 template <int KIND, bool FP8, int WM, int WN, int MBW, int NBW>
-hipError_t launch_one(const GemmParams& p, int R, int E, hipStream_t stream) {
+hipError_t launch_reg(const GemmParams& p, int R, int E, hipStream_t stream) {
   constexpr int BM = WM * MBW * 32;
   constexpr int BN = WN * NBW * 32;
-  // worst case M-tiles over any routing of R rows onto at most min(E, R) experts
-  const long long mt = (long long)(R + BM - 1) / BM + (E < R ? E : R);
-  const long long grid = mt * (p.N / BN);
+  const long long grid = grid_tiles(R, E, BM, BN, p.N);
   if (grid <= 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
   hipLaunchKernelGGL((grouped_gemm_kernel<KIND, FP8, WM, WN, MBW, NBW>), dim3((unsigned)grid),
                      dim3(WM * WN * kWave), 0, stream, p);
+  return hipGetLastError();
+}
+
+template <int KIND, int BK, int STAGES>
+hipError_t launch_dma(const GemmParams& p, int R, int E, hipStream_t stream) {
+  const long long grid = grid_tiles(R, E, 256, 256, p.N);
+  if (grid <= 0) return hipSuccess;
+  if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((grouped_gemm_dma_kernel<KIND, BK, STAGES>), dim3((unsigned)grid), dim3(256),
+                     0, stream, p);
   return hipGetLastError();
 }
 
@@ -380,19 +665,17 @@ template <int KIND, bool FP8>
 hipError_t launch_kind(const GemmParams& p, int R, int E, bool small_m, hipStream_t stream) {
   const bool n256 = (p.N % 256) == 0;
   if (small_m) {
-    if (n256) return launch_one<KIND, FP8, 1, 4, 4, 2>(p, R, E, stream);
-    return launch_one<KIND, FP8, 1, 2, 4, 2>(p, R, E, stream);
+    if (n256) return launch_reg<KIND, FP8, 1, 4, 4, 2>(p, R, E, stream);
+    return launch_reg<KIND, FP8, 1, 2, 4, 2>(p, R, E, stream);
+  }
+  if constexpr (!FP8) {
+    if (n256) return launch_dma<KIND, 32, 4>(p, R, E, stream);
   }
   // fp8 keeps a second (partial-sum) accumulator set, so its tile is half as wide
-  if constexpr (!FP8) {
-    if (n256) return launch_one<KIND, FP8, 2, 2, 4, 4>(p, R, E, stream);
-  }
-  return launch_one<KIND, FP8, 2, 2, 4, 2>(p, R, E, stream);
+  return launch_reg<KIND, FP8, 2, 2, 4, 2>(p, R, E, stream);
 }
 
-}  // namespace
-
-static GemmParams common_params(const FfnArgs& a) {
+GemmParams common_params(const FfnArgs& a) {
   GemmParams g{};
   g.perm = a.perm;
   g.k = a.k;
@@ -405,10 +688,12 @@ static GemmParams common_params(const FfnArgs& a) {
   return g;
 }
 
-static bool small_rows(const FfnArgs& a) {
+bool small_rows(const FfnArgs& a) {
   // decode-sized batches: about one 128-row tile per resident expert or less
   return (long long)a.T * a.k <= 128LL * a.E;
 }
+
+}  // namespace
 
 hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
   // [R,H] x [2I,H]^T -> h [R,I]
