@@ -255,20 +255,21 @@ struct DmaSrc {
   int wave;
 };
 
-template <int KIND, int BK, int STAGES, int BM, int BN, int MBW, int NBW, bool FULL>
+template <int KIND, int BK, int STAGES, int NW, int BM, int BN, int MBW, int NBW, bool FULL>
 struct DmaLoop {
   static constexpr int RB = BK * 2;          // bytes per LDS row
   static constexpr int CH = RB / 16;         // 16-byte chunks per row
   static constexpr int RPI = kWave / CH;     // rows per wave DMA instruction (1 KiB)
-  static constexpr int A_INST = BM / (4 * RPI);
-  static constexpr int B_INST = BN / (4 * RPI);
+  static constexpr int A_INST = BM / (NW * RPI);
+  static constexpr int B_INST = BN / (NW * RPI);
+  static_assert(A_INST * NW * RPI == BM && B_INST * NW * RPI == BN, "DMA rows per wave");
   static constexpr int INST = A_INST + B_INST;
   static constexpr int A_BYTES = BM * RB;
   static constexpr int STAGE_BYTES = (BM + BN) * RB;
   static constexpr int KK = BK / 16;         // MFMA k-steps per tile
   static_assert(KK % 2 == 0, "fragment double buffering alternates sets");
   static_assert(STAGES >= 2 && STAGES <= 4, "ring depth");
-  static_assert(INST % MBW == 0, "DMA instructions spread evenly over row blocks");
+  static_assert(INST % MBW == 0 || MBW % INST == 0, "DMA instructions spread over row blocks");
 
   struct Frags {
     bf16x8 a[MBW];
@@ -281,10 +282,10 @@ struct DmaLoop {
   static __device__ __forceinline__ void issue_one(const Src& s, uint32_t dst, int kt, int q) {
     const int k0b = kt * BK * 2;
     if (q < A_INST)
-      dma16(s.a + k0b, s.a_off[q], dst + (s.wave * (BM / 4) + q * RPI) * RB);
+      dma16(s.a + k0b, s.a_off[q], dst + (s.wave * (BM / NW) + q * RPI) * RB);
     else
       dma16(s.b + k0b, s.b_off[q - A_INST],
-            dst + A_BYTES + (s.wave * (BN / 4) + (q - A_INST) * RPI) * RB);
+            dst + A_BYTES + (s.wave * (BN / NW) + (q - A_INST) * RPI) * RB);
   }
 
   static __device__ __forceinline__ void issue(const Src& s, uint32_t dst, int kt) {
@@ -360,9 +361,13 @@ struct DmaLoop {
             load_a(src, coff(kk + 1), i, a_lane_off, mb_live, fb);
             mma_row(fa, i, mb_live, acc);
             if (kk == 0 && refill) {
+              if constexpr (INST >= MBW) {
 #pragma unroll
-              for (int q = i * (INST / MBW); q < (i + 1) * (INST / MBW); ++q)
-                issue_one(s, dst, nx, q);
+                for (int q = i * (INST / MBW); q < (i + 1) * (INST / MBW); ++q)
+                  issue_one(s, dst, nx, q);
+              } else if (i % (MBW / INST) == 0) {
+                issue_one(s, dst, nx, i / (MBW / INST));
+              }
             }
           }
         } else {
@@ -385,14 +390,17 @@ struct DmaLoop {
   }
 };
 
-template <int KIND, int BK, int STAGES>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+template <int KIND, int BK, int STAGES, int WM, int WN, int MBW, int NBW>
+__global__ __launch_bounds__(WM * WN * kWave)
+__attribute__((amdgpu_waves_per_eu(WM * WN / 4, WM * WN / 4)))
 void grouped_gemm_dma_kernel(GemmParams p) {
-  constexpr int WN = 2, MBW = 4, NBW = 4;
-  constexpr int NT = 256, BM = 256, BN = 256;
+  constexpr int NW = WM * WN;
+  constexpr int NT = NW * kWave;
+  constexpr int BM = WM * MBW * 32, BN = WN * NBW * 32;
   constexpr bool GATEUP = KIND == kGateUp;
-  using Full = DmaLoop<KIND, BK, STAGES, BM, BN, MBW, NBW, true>;
-  using Part = DmaLoop<KIND, BK, STAGES, BM, BN, MBW, NBW, false>;
+  static_assert(!GATEUP || (NBW % 2 == 0), "gate/up pairs gate and up blocks");
+  using Full = DmaLoop<KIND, BK, STAGES, NW, BM, BN, MBW, NBW, true>;
+  using Part = DmaLoop<KIND, BK, STAGES, NW, BM, BN, MBW, NBW, false>;
   constexpr int RB = Full::RB, CH = Full::CH, RPI = Full::RPI;
 
   __shared__ __attribute__((aligned(1024))) char smem_raw[STAGES * Full::STAGE_BYTES];
@@ -415,14 +423,14 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   src.b = reinterpret_cast<const char*>(p.b) + (size_t)t.e * p.N * p.K * 2;
 #pragma unroll
   for (int i = 0; i < Full::A_INST; ++i) {
-    const int row = wave * (BM / 4) + i * RPI + drow;
+    const int row = wave * (BM / NW) + i * RPI + drow;
     const int r = t.r0 + (row < t.rows_valid ? row : 0);
     const int src_row = GATEUP ? min(max(p.perm[r], 0), p.R - 1) / p.k : r;
     src.a_off[i] = (uint32_t)(src_row * p.lda + ((dpc ^ swz<BK>(row)) * 8)) * 2u;
   }
 #pragma unroll
   for (int i = 0; i < Full::B_INST; ++i) {
-    const int j = wave * (BN / 4) + i * RPI + drow;
+    const int j = wave * (BN / NW) + i * RPI + drow;
     src.b_off[i] = (uint32_t)(weight_row<GATEUP, BN>(p, t.tn, j) * p.K + ((dpc ^ swz<BK>(j)) * 8)) * 2u;
   }
 
@@ -649,13 +657,14 @@ hipError_t launch_reg(const GemmParams& p, int R, int E, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int KIND, int BK, int STAGES>
+template <int KIND, int BK, int STAGES, int WM, int WN, int MBW, int NBW>
 hipError_t launch_dma(const GemmParams& p, int R, int E, hipStream_t stream) {
-  const long long grid = grid_tiles(R, E, 256, 256, p.N);
+  constexpr int BM = WM * MBW * 32, BN = WN * NBW * 32;
+  const long long grid = grid_tiles(R, E, BM, BN, p.N);
   if (grid <= 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((grouped_gemm_dma_kernel<KIND, BK, STAGES>), dim3((unsigned)grid), dim3(256),
-                     0, stream, p);
+  hipLaunchKernelGGL((grouped_gemm_dma_kernel<KIND, BK, STAGES, WM, WN, MBW, NBW>),
+                     dim3((unsigned)grid), dim3(WM * WN * kWave), 0, stream, p);
   return hipGetLastError();
 }
 
@@ -669,7 +678,7 @@ hipError_t launch_kind(const GemmParams& p, int R, int E, bool small_m, hipStrea
     return launch_reg<KIND, FP8, 1, 2, 4, 2>(p, R, E, stream);
   }
   if constexpr (!FP8) {
-    if (n256) return launch_dma<KIND, 32, 4>(p, R, E, stream);
+    if (n256) return launch_dma<KIND, 64, 2, 2, 4, 4, 2>(p, R, E, stream);
   }
   // fp8 keeps a second (partial-sum) accumulator set, so its tile is half as wide
   return launch_reg<KIND, FP8, 2, 2, 4, 2>(p, R, E, stream);
