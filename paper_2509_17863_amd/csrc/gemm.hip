@@ -255,21 +255,43 @@ struct DmaSrc {
   int wave;
 };
 
-template <int KIND, int BK, int STAGES, int NW, int BM, int BN, int MBW, int NBW, bool FULL>
+// 8 fp8-e4m3 values -> 8 bf16 (exact).
+__device__ __forceinline__ bf16x8 fp8x8_to_bf16(u32x2 q) {
+  bf16x2 v0 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(q[0], 1.0f, false);
+  bf16x2 v1 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(q[0], 1.0f, true);
+  bf16x2 v2 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(q[1], 1.0f, false);
+  bf16x2 v3 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(q[1], 1.0f, true);
+  return bf16x8{v0[0], v0[1], v1[0], v1[1], v2[0], v2[1], v3[0], v3[1]};
+}
+
+template <int KIND, int BK, int STAGES, int NW, int BM, int BN, int MBW, int NBW, bool FULL,
+          bool FP8>
 struct DmaLoop {
-  static constexpr int RB = BK * 2;          // bytes per LDS row
-  static constexpr int CH = RB / 16;         // 16-byte chunks per row
-  static constexpr int RPI = kWave / CH;     // rows per wave DMA instruction (1 KiB)
-  static constexpr int A_INST = BM / (NW * RPI);
-  static constexpr int B_INST = BN / (NW * RPI);
-  static_assert(A_INST * NW * RPI == BM && B_INST * NW * RPI == BN, "DMA rows per wave");
+  static constexpr int RB = BK * 2;            // bytes per LDS row of A (bf16)
+  static constexpr int CH = RB / 16;           // 16-byte chunks per A row
+  static constexpr int RPI = kWave / CH;       // A rows per wave DMA instruction (1 KiB)
+  static constexpr int BRB = FP8 ? BK : 2 * BK;  // bytes per LDS row of B
+  static constexpr int BCH = BRB / 16;
+  static constexpr int BRPI = kWave / BCH;
+  // DMA instruction g (of NA for A, NB for B) covers rows [g*RPI, (g+1)*RPI);
+  // wave w issues g = w + NW*q.  When NW does not divide NA, the surplus
+  // slots repeat the last instruction (rewriting identical bytes), so every
+  // wave issues the same count and the vmcnt arithmetic stays uniform.
+  static constexpr int NA = BM / RPI;
+  static constexpr int NB = BN / BRPI;
+  static_assert(NA * RPI == BM && NB * BRPI == BN, "DMA rows");
+  static constexpr int A_INST = (NA + NW - 1) / NW;
+  static constexpr int B_INST = (NB + NW - 1) / NW;
+  static __device__ __forceinline__ int a_inst(int wave, int q) { return min(wave + NW * q, NA - 1); }
+  static __device__ __forceinline__ int b_inst(int wave, int q) { return min(wave + NW * q, NB - 1); }
   static constexpr int INST = A_INST + B_INST;
   static constexpr int A_BYTES = BM * RB;
-  static constexpr int STAGE_BYTES = (BM + BN) * RB;
-  static constexpr int KK = BK / 16;         // MFMA k-steps per tile
+  static constexpr int STAGE_BYTES = A_BYTES + BN * BRB;
+  static constexpr int KK = BK / 16;           // MFMA k-steps per tile
+  static constexpr int TILES_PER_SCALE = 128 / BK;  // fp8: K tiles per scale block
   static_assert(KK % 2 == 0, "fragment double buffering alternates sets");
   static_assert(STAGES >= 2 && STAGES <= 4, "ring depth");
-  static_assert(INST % MBW == 0 || MBW % INST == 0, "DMA instructions spread over row blocks");
+  static_assert(!FP8 || 128 % BK == 0, "fp8 scale blocks hold whole K tiles");
 
   struct Frags {
     bf16x8 a[MBW];
@@ -280,12 +302,11 @@ struct DmaLoop {
 
   // DMA instruction q (0..INST-1) of K tile kt into the LDS stage at `dst`.
   static __device__ __forceinline__ void issue_one(const Src& s, uint32_t dst, int kt, int q) {
-    const int k0b = kt * BK * 2;
     if (q < A_INST)
-      dma16(s.a + k0b, s.a_off[q], dst + (s.wave * (BM / NW) + q * RPI) * RB);
+      dma16(s.a + kt * BK * 2, s.a_off[q], dst + a_inst(s.wave, q) * RPI * RB);
     else
-      dma16(s.b + k0b, s.b_off[q - A_INST],
-            dst + A_BYTES + (s.wave * (BN / NW) + (q - A_INST) * RPI) * RB);
+      dma16(s.b + kt * BRB, s.b_off[q - A_INST],
+            dst + A_BYTES + b_inst(s.wave, q - A_INST) * BRPI * BRB);
   }
 
   static __device__ __forceinline__ void issue(const Src& s, uint32_t dst, int kt) {
@@ -293,11 +314,23 @@ struct DmaLoop {
     for (int q = 0; q < INST; ++q) issue_one(s, dst, kt, q);
   }
 
-  static __device__ __forceinline__ void load_b(const LDS_AS char* src, int coff,
-                                                const int (&b_lane_off)[NBW], Frags& f) {
+  // B fragment of k-step kk: bf16 rows use the A layout; fp8 rows are 64 bytes
+  // (16-byte chunk kk, 8-byte half per lane half), converted to bf16 here.
+  static __device__ __forceinline__ void load_b(const LDS_AS char* src, int kk, int coff,
+                                                const int (&b_lane_off)[NBW], int sb_l,
+                                                Frags& f) {
+    if constexpr (FP8) {
+      const int khalf = (threadIdx.x & 63) >> 5;
+      const int boff = ((kk ^ sb_l) << 4) + khalf * 8;
 #pragma unroll
-    for (int j = 0; j < NBW; ++j)
-      f.b[j] = *reinterpret_cast<const LDS_AS bf16x8*>(src + A_BYTES + b_lane_off[j] + coff);
+      for (int j = 0; j < NBW; ++j)
+        f.b[j] = fp8x8_to_bf16(
+            *reinterpret_cast<const LDS_AS u32x2*>(src + A_BYTES + b_lane_off[j] + boff));
+    } else {
+#pragma unroll
+      for (int j = 0; j < NBW; ++j)
+        f.b[j] = *reinterpret_cast<const LDS_AS bf16x8*>(src + A_BYTES + b_lane_off[j] + coff);
+    }
   }
 
   static __device__ __forceinline__ void load_a(const LDS_AS char* src, int coff, int i,
@@ -306,12 +339,16 @@ struct DmaLoop {
       f.a[i] = *reinterpret_cast<const LDS_AS bf16x8*>(src + a_lane_off + i * 32 * RB + coff);
   }
 
+  // MFMAs of row block i; ZERO starts the accumulation from 0 (the first
+  // k-step of an fp8 scale block) instead of reading the accumulator.
+  template <bool ZERO = false>
   static __device__ __forceinline__ void mma_row(const Frags& f, int i, int mb_live,
                                                  f32x16 (&acc)[MBW][NBW]) {
     if (FULL || i < mb_live)
 #pragma unroll
       for (int j = 0; j < NBW; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i],
+                                                            ZERO ? f32x16{} : acc[i][j], 0, 0, 0);
   }
 
   // wait until this wave's DMA of a tile has landed, `later` tiles (issued
@@ -330,67 +367,109 @@ struct DmaLoop {
   //     kt+1, barrier, first fragments of tile kt+1), then the other half.
   // The barrier also certifies that every wave finished reading tile kt, so
   // its stage may be refilled during tile kt+1.
-  static __device__ __forceinline__ void run(const LDS_AS char* smem, const Src& s, int nk,
-                                             int a_lane_off, const int (&b_lane_off)[NBW],
-                                             int s_l, int mb_live, f32x16 (&acc)[MBW][NBW]) {
+  // fp8: MFMAs accumulate the current 128-wide K block in `mac`, which is
+  // scaled by the block's scale (per N block, sc[j] + kb) and added to `acc`.
+  // One K tile (see run()).  FRESH: the tile starts an fp8 scale block, so its
+  // first k-step overwrites the partial sums instead of accumulating.
+  template <bool FRESH>
+  static __device__ __forceinline__ void tile(const LDS_AS char* smem, const Src& s, int nk,
+                                              int kt, int a_lane_off,
+                                              const int (&b_lane_off)[NBW], int s_l, int sb_l,
+                                              int mb_live, Frags (&f)[2],
+                                              f32x16 (&mac)[MBW][NBW]) {
     const int khalf = (threadIdx.x & 63) >> 5;
     auto coff = [&](int kk) { return (((2 * kk + khalf) ^ s_l) << 4); };
+    const LDS_AS char* src = smem + (kt % STAGES) * STAGE_BYTES;
+    const int nx = kt + STAGES - 1;
+    const bool refill = nx < nk;
+    const uint32_t dst = s.lds + (nx % STAGES) * STAGE_BYTES;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      Frags& fa = f[kk & 1];
+      Frags& fb = f[(kk + 1) & 1];
+      if (kk + 1 < KK) {
+        load_b(src, kk + 1, coff(kk + 1), b_lane_off, sb_l, fb);
+#pragma unroll
+        for (int i = 0; i < MBW; ++i) {
+          load_a(src, coff(kk + 1), i, a_lane_off, mb_live, fb);
+          if (FRESH && kk == 0) mma_row<true>(fa, i, mb_live, mac);
+          else mma_row(fa, i, mb_live, mac);
+          if (kk == 0 && refill) {
+            // spread the INST DMA instructions over the MBW row blocks
+#pragma unroll
+            for (int q = i * INST / MBW; q < (i + 1) * INST / MBW; ++q) issue_one(s, dst, nx, q);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < MBW / 2; ++i) mma_row(fa, i, mb_live, mac);
+        if (kt + 1 < nk) {
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+          wait_tiles(min(STAGES - 2, nk - 2 - kt));
+          lds_barrier();
+          const LDS_AS char* nsrc = smem + ((kt + 1) % STAGES) * STAGE_BYTES;
+          load_b(nsrc, 0, coff(0), b_lane_off, sb_l, fb);
+#pragma unroll
+          for (int i = 0; i < MBW; ++i) load_a(nsrc, coff(0), i, a_lane_off, mb_live, fb);
+        }
+#pragma unroll
+        for (int i = MBW / 2; i < MBW; ++i) mma_row(fa, i, mb_live, mac);
+      }
+    }
+  }
+
+  // Software pipeline over K tiles (tile kt lives in stage kt % STAGES):
+  //   k-step 0 of tile kt: its MFMAs interleaved with the DMA of tile
+  //     kt+STAGES-1 (into the stage tile kt-1 used, released by the previous
+  //     barrier) and the fragment reads of the next k-step;
+  //   last k-step: half the MFMAs, then the tile boundary (wait for tile
+  //     kt+1, barrier, first fragments of tile kt+1), then the other half.
+  // The barrier also certifies that every wave finished reading tile kt, so
+  // its stage may be refilled during tile kt+1.
+  // fp8: the MFMAs of one 128-wide K block (TILES_PER_SCALE tiles) go to
+  // `part`, which is then scaled by the block's scale (per N block,
+  // sc[j][kb]) and added to `acc`.
+  static __device__ __forceinline__ void run(const LDS_AS char* smem, const Src& s, int nk,
+                                             int a_lane_off, const int (&b_lane_off)[NBW],
+                                             int s_l, int sb_l, int mb_live,
+                                             const float* const (&sc)[NBW],
+                                             f32x16 (&acc)[MBW][NBW]) {
+    const int khalf = (threadIdx.x & 63) >> 5;
+    const int coff0 = ((khalf ^ s_l) << 4);
 #pragma unroll
     for (int t = 0; t < STAGES - 1; ++t)
       if (t < nk) issue(s, s.lds + t * STAGE_BYTES, t);
     wait_tiles(min(STAGES - 2, nk - 1));
     lds_barrier();
     Frags f[2];
-    load_b(smem, coff(0), b_lane_off, f[0]);
+    load_b(smem, 0, coff0, b_lane_off, sb_l, f[0]);
 #pragma unroll
-    for (int i = 0; i < MBW; ++i) load_a(smem, coff(0), i, a_lane_off, mb_live, f[0]);
+    for (int i = 0; i < MBW; ++i) load_a(smem, coff0, i, a_lane_off, mb_live, f[0]);
 
-    for (int kt = 0; kt < nk; ++kt) {
-      const LDS_AS char* src = smem + (kt % STAGES) * STAGE_BYTES;
-      const int nx = kt + STAGES - 1;
-      const bool refill = nx < nk;
-      const uint32_t dst = s.lds + (nx % STAGES) * STAGE_BYTES;
+    if constexpr (FP8) {
+      f32x16 part[MBW][NBW];
+      for (int kt = 0; kt < nk; kt += TILES_PER_SCALE) {
+        tile<true>(smem, s, nk, kt, a_lane_off, b_lane_off, s_l, sb_l, mb_live, f, part);
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        Frags& fa = f[kk & 1];
-        Frags& fb = f[(kk + 1) & 1];
-        if (kk + 1 < KK) {
-          load_b(src, coff(kk + 1), b_lane_off, fb);
+        for (int u = 1; u < TILES_PER_SCALE; ++u)
+          tile<false>(smem, s, nk, kt + u, a_lane_off, b_lane_off, s_l, sb_l, mb_live, f, part);
+        const int kb = kt / TILES_PER_SCALE;
 #pragma unroll
-          for (int i = 0; i < MBW; ++i) {
-            load_a(src, coff(kk + 1), i, a_lane_off, mb_live, fb);
-            mma_row(fa, i, mb_live, acc);
-            if (kk == 0 && refill) {
-              if constexpr (INST >= MBW) {
+        for (int j = 0; j < NBW; ++j) {
+          const float scale = sc[j][kb];
 #pragma unroll
-                for (int q = i * (INST / MBW); q < (i + 1) * (INST / MBW); ++q)
-                  issue_one(s, dst, nx, q);
-              } else if (i % (MBW / INST) == 0) {
-                issue_one(s, dst, nx, i / (MBW / INST));
-              }
-            }
-          }
-        } else {
-#pragma unroll
-          for (int i = 0; i < MBW / 2; ++i) mma_row(fa, i, mb_live, acc);
-          if (kt + 1 < nk) {
-            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-            wait_tiles(min(STAGES - 2, nk - 2 - kt));
-            lds_barrier();
-            const LDS_AS char* nsrc = smem + ((kt + 1) % STAGES) * STAGE_BYTES;
-            load_b(nsrc, coff(0), b_lane_off, fb);
-#pragma unroll
-            for (int i = 0; i < MBW; ++i) load_a(nsrc, coff(0), i, a_lane_off, mb_live, fb);
-          }
-#pragma unroll
-          for (int i = MBW / 2; i < MBW; ++i) mma_row(fa, i, mb_live, acc);
+          for (int i = 0; i < MBW; ++i)
+            if (FULL || i < mb_live) acc[i][j] += scale * part[i][j];
         }
       }
+    } else {
+      for (int kt = 0; kt < nk; ++kt)
+        tile<false>(smem, s, nk, kt, a_lane_off, b_lane_off, s_l, sb_l, mb_live, f, acc);
     }
   }
 };
 
-template <int KIND, int BK, int STAGES, int WM, int WN, int MBW, int NBW>
+template <int KIND, bool FP8, int BK, int STAGES, int WM, int WN, int MBW, int NBW>
 __global__ __launch_bounds__(WM * WN * kWave)
 __attribute__((amdgpu_waves_per_eu(WM * WN / 4, WM * WN / 4)))
 void grouped_gemm_dma_kernel(GemmParams p) {
@@ -399,9 +478,10 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   constexpr int BM = WM * MBW * 32, BN = WN * NBW * 32;
   constexpr bool GATEUP = KIND == kGateUp;
   static_assert(!GATEUP || (NBW % 2 == 0), "gate/up pairs gate and up blocks");
-  using Full = DmaLoop<KIND, BK, STAGES, NW, BM, BN, MBW, NBW, true>;
-  using Part = DmaLoop<KIND, BK, STAGES, NW, BM, BN, MBW, NBW, false>;
+  using Full = DmaLoop<KIND, BK, STAGES, NW, BM, BN, MBW, NBW, true, FP8>;
+  using Part = DmaLoop<KIND, BK, STAGES, NW, BM, BN, MBW, NBW, false, FP8>;
   constexpr int RB = Full::RB, CH = Full::CH, RPI = Full::RPI;
+  constexpr int BRB = Full::BRB, BCH = Full::BCH, BRPI = Full::BRPI;
 
   __shared__ __attribute__((aligned(1024))) char smem_raw[STAGES * Full::STAGE_BYTES];
   __shared__ int s_tp[kMaxExperts + 1];
@@ -414,24 +494,32 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   // DMA: lane writes 16 bytes at (row lane/CH, physical chunk lane%CH) of its
-  // instruction's RPI rows, so it fetches logical chunk (lane%CH) ^ swz(row)
-  const int drow = lane / CH;
-  const int dpc = lane % CH;
+  // instruction's rows, so it fetches logical chunk (lane%CH) ^ swizzle(row)
   typename Full::Src src;
   src.wave = wave;
   src.a = reinterpret_cast<const char*>(p.a);
-  src.b = reinterpret_cast<const char*>(p.b) + (size_t)t.e * p.N * p.K * 2;
+  src.b = reinterpret_cast<const char*>(p.b) + (size_t)t.e * p.N * p.K * (FP8 ? 1 : 2);
+  {
+    const int drow = lane / CH;
+    const int dpc = lane % CH;
 #pragma unroll
-  for (int i = 0; i < Full::A_INST; ++i) {
-    const int row = wave * (BM / NW) + i * RPI + drow;
-    const int r = t.r0 + (row < t.rows_valid ? row : 0);
-    const int src_row = GATEUP ? min(max(p.perm[r], 0), p.R - 1) / p.k : r;
-    src.a_off[i] = (uint32_t)(src_row * p.lda + ((dpc ^ swz<BK>(row)) * 8)) * 2u;
+    for (int i = 0; i < Full::A_INST; ++i) {
+      const int row = Full::a_inst(wave, i) * RPI + drow;
+      const int r = t.r0 + (row < t.rows_valid ? row : 0);
+      const int src_row = GATEUP ? min(max(p.perm[r], 0), p.R - 1) / p.k : r;
+      src.a_off[i] = (uint32_t)(src_row * p.lda + ((dpc ^ swz<BK>(row)) * 8)) * 2u;
+    }
   }
+  {
+    const int drow = lane / BCH;
+    const int dpc = lane % BCH;
 #pragma unroll
-  for (int i = 0; i < Full::B_INST; ++i) {
-    const int j = wave * (BN / NW) + i * RPI + drow;
-    src.b_off[i] = (uint32_t)(weight_row<GATEUP, BN>(p, t.tn, j) * p.K + ((dpc ^ swz<BK>(j)) * 8)) * 2u;
+    for (int i = 0; i < Full::B_INST; ++i) {
+      const int j = Full::b_inst(wave, i) * BRPI + drow;
+      const int chunk = dpc ^ (FP8 ? swz<32>(j) : swz<BK>(j));
+      src.b_off[i] = (uint32_t)weight_row<GATEUP, BN>(p, t.tn, j) * (uint32_t)p.K * (FP8 ? 1u : 2u) +
+                     (uint32_t)chunk * 16u;
+    }
   }
 
   const int wm = wave / WN;
@@ -440,9 +528,17 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   const int am0 = wm * MBW * 32;
   const int a_lane_off = (am0 + lrow) * RB;
   int b_lane_off[NBW];
+  const float* sc[NBW];
 #pragma unroll
-  for (int j = 0; j < NBW; ++j) b_lane_off[j] = (block_row<GATEUP, BN, NBW>(wn, j) + lrow) * RB;
+  for (int j = 0; j < NBW; ++j) {
+    const int br = block_row<GATEUP, BN, NBW>(wn, j);
+    b_lane_off[j] = (br + lrow) * BRB;
+    sc[j] = FP8 ? p.b_scale + ((size_t)t.e * (p.N / 128) + weight_row<GATEUP, BN>(p, t.tn, br) / 128) *
+                                  (p.K / 128)
+                : nullptr;
+  }
   const int s_l = swz<BK>(lrow);
+  const int sb_l = swz<32>(lrow);
   const int mb_live =
       __builtin_amdgcn_readfirstlane(max(0, min(MBW, ceil_div(t.rows_valid - am0, 32))));
 
@@ -456,9 +552,9 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   src.lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
   const int nk = p.K / BK;
   if (t.rows_valid == BM)
-    Full::run(smem, src, nk, a_lane_off, b_lane_off, s_l, mb_live, acc);
+    Full::run(smem, src, nk, a_lane_off, b_lane_off, s_l, sb_l, mb_live, sc, acc);
   else
-    Part::run(smem, src, nk, a_lane_off, b_lane_off, s_l, mb_live, acc);
+    Part::run(smem, src, nk, a_lane_off, b_lane_off, s_l, sb_l, mb_live, sc, acc);
 
   epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, acc);
 }
@@ -657,31 +753,42 @@ hipError_t launch_reg(const GemmParams& p, int R, int E, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int KIND, int BK, int STAGES, int WM, int WN, int MBW, int NBW>
+template <int KIND, bool FP8, int BK, int STAGES, int WM, int WN, int MBW, int NBW>
 hipError_t launch_dma(const GemmParams& p, int R, int E, hipStream_t stream) {
   constexpr int BM = WM * MBW * 32, BN = WN * NBW * 32;
   const long long grid = grid_tiles(R, E, BM, BN, p.N);
   if (grid <= 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((grouped_gemm_dma_kernel<KIND, BK, STAGES, WM, WN, MBW, NBW>),
+  hipLaunchKernelGGL((grouped_gemm_dma_kernel<KIND, FP8, BK, STAGES, WM, WN, MBW, NBW>),
                      dim3((unsigned)grid), dim3(WM * WN * kWave), 0, stream, p);
   return hipGetLastError();
 }
 
-// Tile shapes: prefill-sized batches take 256x256 tiles (4 waves of 128x128);
-// decode-sized batches (few rows per expert) take 128-row tiles.
+// Tile shapes (N a multiple of 256 takes the LDS-DMA kernels):
+//   bf16, prefill-sized: 256x256 tiles, 8 waves of 128x64, BK=64, 2 stages;
+//   fp8 weights: 96x512 tiles (a decode batch's ~50-90 rows per expert fit
+//     one tile, so the weights stream once), 8 waves of 96x64 -- two per
+//     SIMD, so one wave's partial-sum scaling (VALU) overlaps the other's
+//     MFMAs -- BK=64, 3 stages so 64 KiB of weights per CU are in flight
+//     while a tile is multiplied (96x256 with 4 waves when N is not a
+//     multiple of 512);
+//   decode-sized bf16 and other N: register-staged 128-row tiles.
 template <int KIND, bool FP8>
 hipError_t launch_kind(const GemmParams& p, int R, int E, bool small_m, hipStream_t stream) {
   const bool n256 = (p.N % 256) == 0;
-  if (small_m) {
-    if (n256) return launch_reg<KIND, FP8, 1, 4, 4, 2>(p, R, E, stream);
-    return launch_reg<KIND, FP8, 1, 2, 4, 2>(p, R, E, stream);
+  if constexpr (FP8) {
+    if (p.N % 512 == 0) return launch_dma<KIND, true, 64, 3, 1, 8, 3, 2>(p, R, E, stream);
+    if (n256) return launch_dma<KIND, true, 64, 3, 1, 4, 3, 2>(p, R, E, stream);
+    if (small_m) return launch_reg<KIND, true, 1, 2, 4, 2>(p, R, E, stream);
+    return launch_reg<KIND, true, 2, 2, 4, 2>(p, R, E, stream);
+  } else {
+    if (small_m) {
+      if (n256) return launch_reg<KIND, false, 1, 4, 4, 2>(p, R, E, stream);
+      return launch_reg<KIND, false, 1, 2, 4, 2>(p, R, E, stream);
+    }
+    if (n256) return launch_dma<KIND, false, 64, 2, 2, 4, 4, 2>(p, R, E, stream);
+    return launch_reg<KIND, false, 2, 2, 4, 2>(p, R, E, stream);
   }
-  if constexpr (!FP8) {
-    if (n256) return launch_dma<KIND, 64, 2, 2, 4, 4, 2>(p, R, E, stream);
-  }
-  // fp8 keeps a second (partial-sum) accumulator set, so its tile is half as wide
-  return launch_reg<KIND, FP8, 2, 2, 4, 2>(p, R, E, stream);
 }
 
 GemmParams common_params(const FfnArgs& a) {
