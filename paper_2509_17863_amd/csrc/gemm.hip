@@ -29,10 +29,10 @@
 //
 // Scheduling: the workgroup reads the compacted active list (group-shrink)
 // into LDS once and builds the per-expert M-tile prefix there.  Tile ids are
-// ordered expert-major, then weight N-tile, then M-tile, so the M-tiles that
-// share one weight tile run back to back; workgroup ids are remapped so each
-// XCD (ids congruent mod 8) gets a contiguous range of tiles and its L2 sees
-// that reuse.  The grid is sized for the worst case from R and E alone (no
+// ordered expert-major, then in groups of 8 M-tiles, N-tile major and M-tile
+// minor inside a group, so tiles that run together share weight and token
+// tiles; workgroup ids are remapped so each XCD (ids congruent mod 8) gets a
+// contiguous range of tiles and its L2 sees that reuse.  The grid is sized for the worst case from R and E alone (no
 // host readback); surplus workgroups exit after the prologue.
 #include "common.h"
 #include "internal.h"
@@ -43,6 +43,7 @@ namespace {
 #define LDS_AS __attribute__((address_space(3)))
 
 constexpr int kNumXcd = 8;
+constexpr int kGroupM = 8;  // M-tiles per ordering group inside an expert
 
 enum GemmKind { kGateUp = 0, kDownPlainK = 1, kDownWeightedK = 2 };
 
@@ -72,8 +73,10 @@ struct Tile {
   int rows_valid;  // rows of the tile that belong to the expert
 };
 
+// silu(g) * u with the hardware exp and reciprocal (a few ulp from the
+// correctly rounded value, which moves rare h roundings by one bf16 ulp).
 __device__ __forceinline__ float silu_mul(float g, float u) {
-  return g / (1.0f + __expf(-g)) * u;
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
 }
 
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
@@ -149,9 +152,15 @@ __device__ __forceinline__ bool locate_tile(const GemmParams& p, int* s_tp, int*
   const int e = s_exp[lo];
   const int mt = s_tp[lo + 1] - s_tp[lo];
   const int local = tile - s_tp[lo] * n_tiles_n;
+  // inside an expert, tiles go in groups of kGroupM M-tiles: N-tile major,
+  // M-tile minor within a group, so any 32 consecutive tiles (one XCD's
+  // workgroups at a time) cover <= 8 M-tiles x >= 4 N-tiles and share operands
+  const int g = local / (kGroupM * n_tiles_n);
+  const int gm = min(kGroupM, mt - g * kGroupM);
+  const int lg = local - g * kGroupM * n_tiles_n;
   t.e = e;
-  t.tn = local / mt;
-  const int tm = local - t.tn * mt;
+  t.tn = lg / gm;
+  const int tm = g * kGroupM + (lg - t.tn * gm);
   const int beg = min(max(p.offsets[e], 0), p.R);
   const int end = min(max(p.offsets[e + 1], beg), p.R);
   t.r0 = beg + tm * BM;
@@ -176,11 +185,39 @@ __device__ __forceinline__ int block_row(int wn, int j) {
   return wn * NBW * 32 + j * 32;
 }
 
+// Output row and router weight of each of the lane's token rows, loaded
+// before the main loop so the epilogue's stores do not wait on them.
+template <int MBW>
+struct RowInfo {
+  int orow[MBW];
+  float wt[MBW];
+};
+
+template <int KIND, int MBW>
+__device__ __forceinline__ RowInfo<MBW> row_info(const GemmParams& p, const Tile& t, int am0,
+                                                 int mb_live) {
+  RowInfo<MBW> ri;
+  const int lrow = threadIdx.x & 31;
+#pragma unroll
+  for (int i = 0; i < MBW; ++i) {
+    const int rr = am0 + i * 32 + lrow;
+    const int r = t.r0 + (rr < t.rows_valid ? rr : 0);
+    ri.orow[i] = r;
+    ri.wt[i] = 1.0f;
+    if (KIND == kDownWeightedK && i < mb_live) {
+      ri.orow[i] = min(max(p.perm[r], 0), p.R - 1);
+      ri.wt[i] = p.w[ri.orow[i]];
+    }
+  }
+  return ri;
+}
+
 // acc[i][j][v]: token row am0 + i*32 + lane%32, weight row
 // block_row(j) + 8*(v/4) + 4*(lane/32) + v%4.
 template <int KIND, int BN, int MBW, int NBW>
 __device__ __forceinline__ void epilogue(const GemmParams& p, const Tile& t, int wn, int am0,
-                                         int mb_live, const f32x16 (&acc)[MBW][NBW]) {
+                                         int mb_live, const RowInfo<MBW>& ri,
+                                         const f32x16 (&acc)[MBW][NBW]) {
   const int lane = threadIdx.x & (kWave - 1);
   const int lrow = lane & 31;
   const int khalf = lane >> 5;
@@ -206,12 +243,8 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, const Tile& t, int
         }
       }
     } else {
-      int orow = r;
-      float wt = 1.0f;
-      if (KIND == kDownWeightedK) {
-        orow = min(max(p.perm[r], 0), p.R - 1);
-        wt = p.w[orow];
-      }
+      const int orow = ri.orow[i];
+      const float wt = ri.wt[i];
       float* yrow = p.y + (size_t)orow * p.N + t.tn * BN + wn * NBW * 32;
 #pragma unroll
       for (int j = 0; j < NBW; ++j) {
@@ -548,6 +581,7 @@ void grouped_gemm_dma_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < NBW; ++j) acc[i][j] = f32x16{};
 
+  const RowInfo<MBW> ri = row_info<KIND, MBW>(p, t, am0, mb_live);
   const LDS_AS char* smem = (const LDS_AS char*)smem_raw;  // generic -> LDS address space
   src.lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
   const int nk = p.K / BK;
@@ -556,7 +590,7 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   else
     Part::run(smem, src, nk, a_lane_off, b_lane_off, s_l, sb_l, mb_live, sc, acc);
 
-  epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, acc);
+  epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, ri, acc);
 }
 
 // ============================================================================
@@ -682,6 +716,7 @@ void grouped_gemm_kernel(GemmParams p) {
       for (int j = 0; j < (FP8 ? NBW : 1); ++j) part[i][j] = f32x16{};
   }
 
+  const RowInfo<MBW> ri = row_info<KIND, MBW>(p, t, am0, mb_live);
   const int nk = p.K / kBK;
   load_global(0);
   store_lds(0);
@@ -732,7 +767,7 @@ void grouped_gemm_kernel(GemmParams p) {
     if (kt + 1 < nk) store_lds(cur ^ 1);
     __syncthreads();
   }
-  epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, acc);
+  epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, ri, acc);
 }
 
 // worst case M-tiles over any routing of R rows onto at most min(E, R) experts
