@@ -7,8 +7,10 @@ weighted epilogue, combine), inputs resident in HBM.  Prints one JSON line.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -40,6 +42,31 @@ def algorithmic(d: dict, counts: np.ndarray) -> dict:
     return dict(flops=6.0 * R * H * I, gu_flops=4.0 * R * H * I, dn_flops=2.0 * R * H * I,
                 gu_bytes=gu_bytes, dn_bytes=dn_bytes,
                 bytes=gu_bytes + dn_bytes - R * I * 2 * 0 + T * k * 4)
+
+
+def kernel_source_sha256() -> str:
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "common.h", "internal.h"):
+        with open(os.path.join(ROOT, "paper_2509_17863_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per gate/up launch from the committed rocprofv3 FETCH_SIZE and
+    WRITE_SIZE runs of this workload, scaled by a copy kernel of known size;
+    None when there is no record or the kernel sources changed since."""
+    path = os.path.join(ROOT, "profiles", f"kernels_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"```json\n(\{.*?\})\n```", text, re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("kernel_source_sha256") != kernel_source_sha256():
+        return None
+    return int(rec["traffic_bytes"])
 
 
 def cpu_baseline(d: dict, target_s: float = 12.0) -> dict:
@@ -144,7 +171,10 @@ def main() -> int:
         achieved = alg["gu_flops"] / (t_gu * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None}
-    roof["kernel"] = "grouped_gemm_kernel<gate/up>"
+    roof["traffic"] = measured_traffic(args.workload)
+    roof["traffic_unit"] = "bytes per launch"
+    roof["algorithmic_bytes"] = int(alg["gu_bytes"])
+    roof["kernel"] = "grouped_gemm_dma_kernel<gate/up>"
     res = {
         "metric": "expert-FFN tokens/s",
         "value": round(T / (ms * 1e-3), 1),

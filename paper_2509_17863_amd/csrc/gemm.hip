@@ -86,9 +86,18 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "me
 // lds + 16*l.  Issued from inline assembly so the compiler adds no waits of
 // its own; completion is tracked with explicit vmcnt waits.  `base` and `lds`
 // are wave-uniform (SGPRs; `lds` goes to M0).
+// The base is passed through readfirstlane so it is held in SGPRs even where
+// the compiler cannot prove it uniform (free when it already is).
+__device__ __forceinline__ const void* wave_uniform(const void* p) {
+  const uint64_t v = reinterpret_cast<uintptr_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<const void*>(((uint64_t)hi << 32) | lo);
+}
+
 __device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-               :: "v"(voff), "s"(base), "s"(lds) : "memory");
+               :: "v"(voff), "s"(wave_uniform(base)), "s"(lds) : "memory");
 }
 
 // Group-shrink schedule: the active list and its M-tile prefix go to LDS once,
