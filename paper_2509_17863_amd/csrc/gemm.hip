@@ -41,6 +41,7 @@ namespace eaas {
 namespace {
 
 #define LDS_AS __attribute__((address_space(3)))
+#define CONST_AS __attribute__((address_space(4)))  // read-only global data, scalar loads
 
 constexpr int kNumXcd = 8;
 constexpr int kGroupM = 8;  // M-tiles per ordering group inside an expert
@@ -280,10 +281,12 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, const Tile& t, int
 // lanes (128-byte bank lines) or 16 lanes (256-byte bank lines) in flight per
 // cycle, reading one chunk column of consecutive rows; the swizzle puts those
 // rows' chunks on distinct banks in both cases.
-template <int BK>
+template <int ROW_BYTES>
 __device__ __forceinline__ int swz(int row) {
-  if (BK == 64) return (row & 7) ^ ((row >> 3) & 1);      // 128-byte rows, 8 chunks
-  return ((row >> 1) & 3) ^ ((row >> 3) & 1);              // 64-byte rows, 4 chunks
+  static_assert(ROW_BYTES == 64 || ROW_BYTES == 128 || ROW_BYTES == 256, "LDS row size");
+  if (ROW_BYTES == 256) return row & 15;                         // 16 chunks
+  if (ROW_BYTES == 128) return (row & 7) ^ ((row >> 3) & 1);     // 8 chunks
+  return ((row >> 1) & 3) ^ ((row >> 3) & 1);                    // 4 chunks
 }
 
 // Global sources of a tile's DMA (shared by the full- and partial-tile loops).
@@ -306,13 +309,16 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16(u32x2 q) {
   return bf16x8{v0[0], v0[1], v1[0], v1[1], v2[0], v2[1], v3[0], v3[1]};
 }
 
-template <int KIND, int BK, int STAGES, int NW, int BM, int BN, int MBW, int NBW, bool FULL,
-          bool FP8>
+template <int KIND, int BK, int SA, int SB, int BSPAN, int NW, int BM, int BN, int MBW, int NBW,
+          bool FULL, bool FP8>
 struct DmaLoop {
   static constexpr int RB = BK * 2;            // bytes per LDS row of A (bf16)
   static constexpr int CH = RB / 16;           // 16-byte chunks per A row
   static constexpr int RPI = kWave / CH;       // A rows per wave DMA instruction (1 KiB)
-  static constexpr int BRB = FP8 ? BK : 2 * BK;  // bytes per LDS row of B
+  // A B stage spans BSPAN K tiles, so an fp8 weight row is fetched as whole
+  // 128-byte lines (BK = 64, BSPAN = 2) while the token rows stay in BK tiles.
+  static constexpr int BTB = FP8 ? BK : 2 * BK;  // bytes of one K tile of a B row
+  static constexpr int BRB = BTB * BSPAN;        // bytes per LDS row of a B stage
   static constexpr int BCH = BRB / 16;
   static constexpr int BRPI = kWave / BCH;
   // DMA instruction g (of NA for A, NB for B) covers rows [g*RPI, (g+1)*RPI);
@@ -327,12 +333,19 @@ struct DmaLoop {
   static __device__ __forceinline__ int a_inst(int wave, int q) { return min(wave + NW * q, NA - 1); }
   static __device__ __forceinline__ int b_inst(int wave, int q) { return min(wave + NW * q, NB - 1); }
   static constexpr int INST = A_INST + B_INST;
+  // LDS: a ring of SA token-row (A) stages, then a ring of SB weight (B)
+  // stages of BSPAN K tiles each.  SB = SA + 1 gives the weights, which come
+  // from HBM, one more K tile of flight time than the token rows, which
+  // mostly hit L2; BSPAN = 2 (with SA = SB = 2) gives them two.
   static constexpr int A_BYTES = BM * RB;
-  static constexpr int STAGE_BYTES = A_BYTES + BN * BRB;
+  static constexpr int B_BYTES = BN * BRB;
+  static constexpr int B_BASE = SA * A_BYTES;
+  static constexpr int LDS_BYTES = SA * A_BYTES + SB * B_BYTES;
   static constexpr int KK = BK / 16;           // MFMA k-steps per tile
   static constexpr int TILES_PER_SCALE = 128 / BK;  // fp8: K tiles per scale block
   static_assert(KK % 2 == 0, "fragment double buffering alternates sets");
-  static_assert(STAGES >= 2 && STAGES <= 4, "ring depth");
+  static_assert(SA >= 2 && SB <= 4 && (SB == SA || (SB == SA + 1 && SA <= 3)), "ring depths");
+  static_assert(BSPAN == 1 || (BSPAN == 2 && FP8 && SA == 2 && SB == 2), "B stage span");
   static_assert(!FP8 || 128 % BK == 0, "fp8 scale blocks hold whole K tiles");
 
   struct Frags {
@@ -342,43 +355,54 @@ struct DmaLoop {
 
   using Src = DmaSrc<A_INST, B_INST>;
 
-  // DMA instruction q (0..INST-1) of K tile kt into the LDS stage at `dst`.
-  static __device__ __forceinline__ void issue_one(const Src& s, uint32_t dst, int kt, int q) {
-    if (q < A_INST)
-      dma16(s.a + kt * BK * 2, s.a_off[q], dst + a_inst(s.wave, q) * RPI * RB);
-    else
-      dma16(s.b + kt * BRB, s.b_off[q - A_INST],
-            dst + A_BYTES + b_inst(s.wave, q - A_INST) * BRPI * BRB);
+  // DMA instruction q (0..INST-1): the A part loads K tile ka, the B part B
+  // stage kb (K tiles kb*BSPAN ..), each into its ring slot; ka >= nk or
+  // kb outside [0, nb) issue nothing.
+  static __device__ __forceinline__ void issue_one(const Src& s, int ka, int kb, int nk, int nb,
+                                                   int q) {
+    if (q < A_INST) {
+      if (ka < nk)
+        dma16(s.a + ka * BK * 2, s.a_off[q],
+              s.lds + (ka % SA) * A_BYTES + a_inst(s.wave, q) * RPI * RB);
+    } else {
+      if (kb >= 0 && kb < nb)
+        dma16(s.b + kb * BRB, s.b_off[q - A_INST],
+              s.lds + B_BASE + (kb % SB) * B_BYTES + b_inst(s.wave, q - A_INST) * BRPI * BRB);
+    }
   }
 
-  static __device__ __forceinline__ void issue(const Src& s, uint32_t dst, int kt) {
+  static __device__ __forceinline__ void issue_a(const Src& s, int kt, int nk) {
 #pragma unroll
-    for (int q = 0; q < INST; ++q) issue_one(s, dst, kt, q);
+    for (int q = 0; q < A_INST; ++q) issue_one(s, kt, -1, nk, 0, q);
+  }
+  static __device__ __forceinline__ void issue_b(const Src& s, int kb, int nb) {
+#pragma unroll
+    for (int q = A_INST; q < INST; ++q) issue_one(s, 0, kb, 0, nb, q);
   }
 
-  // B fragment of k-step kk: bf16 rows use the A layout; fp8 rows are 64 bytes
-  // (16-byte chunk kk, 8-byte half per lane half), converted to bf16 here.
-  static __device__ __forceinline__ void load_b(const LDS_AS char* src, int kk, int coff,
+  // B fragment of k-step kk from the B stage at `bsrc`: bf16 rows use the A
+  // layout; fp8 rows hold BSPAN K tiles of BK bytes (16-byte chunk kk of K
+  // tile part `kp`, 8-byte half per lane half), converted to bf16 here.
+  static __device__ __forceinline__ void load_b(const LDS_AS char* bsrc, int kk, int kp, int coff,
                                                 const int (&b_lane_off)[NBW], int sb_l,
                                                 Frags& f) {
     if constexpr (FP8) {
       const int khalf = (threadIdx.x & 63) >> 5;
-      const int boff = ((kk ^ sb_l) << 4) + khalf * 8;
+      const int boff = (((kp * KK + kk) ^ sb_l) << 4) + khalf * 8;
 #pragma unroll
       for (int j = 0; j < NBW; ++j)
-        f.b[j] = fp8x8_to_bf16(
-            *reinterpret_cast<const LDS_AS u32x2*>(src + A_BYTES + b_lane_off[j] + boff));
+        f.b[j] = fp8x8_to_bf16(*reinterpret_cast<const LDS_AS u32x2*>(bsrc + b_lane_off[j] + boff));
     } else {
 #pragma unroll
       for (int j = 0; j < NBW; ++j)
-        f.b[j] = *reinterpret_cast<const LDS_AS bf16x8*>(src + A_BYTES + b_lane_off[j] + coff);
+        f.b[j] = *reinterpret_cast<const LDS_AS bf16x8*>(bsrc + b_lane_off[j] + coff);
     }
   }
 
-  static __device__ __forceinline__ void load_a(const LDS_AS char* src, int coff, int i,
+  static __device__ __forceinline__ void load_a(const LDS_AS char* asrc, int coff, int i,
                                                 int a_lane_off, int mb_live, Frags& f) {
     if (FULL || i < mb_live)
-      f.a[i] = *reinterpret_cast<const LDS_AS bf16x8*>(src + a_lane_off + i * 32 * RB + coff);
+      f.a[i] = *reinterpret_cast<const LDS_AS bf16x8*>(asrc + a_lane_off + i * 32 * RB + coff);
   }
 
   // MFMAs of row block i; ZERO starts the accumulation from 0 (the first
@@ -393,26 +417,42 @@ struct DmaLoop {
                                                             ZERO ? f32x16{} : acc[i][j], 0, 0, 0);
   }
 
-  // wait until this wave's DMA of a tile has landed, `later` tiles (issued
-  // after it) possibly still in flight
-  static __device__ __forceinline__ void wait_tiles(int later) {
-    if (STAGES > 3 && later >= 2) wait_vmcnt<(STAGES > 3 ? 2 * INST : 0)>();
-    else if (STAGES > 2 && later >= 1) wait_vmcnt<(STAGES > 2 ? INST : 0)>();
-    else wait_vmcnt<0>();
+  // Wait until this wave's DMA of K tile kt+1 (both parts) has landed.  Loads
+  // complete in issue order for vmcnt, so the wait allows exactly the
+  // instructions issued after the later of the two parts:
+  //   SA == SB: iteration i issues A(i+S-1) then B(i+S-1); after B(kt+1)
+  //     come the groups of tiles kt+2 .. kt+S-1 (those < nk).
+  //   SB == SA+1: iteration i issues A(i+SA-1) then B(i+SA); after A(kt+1)
+  //     come B(kt+2), then A(kt+2), B(kt+3) when SA == 3 (those < nk).
+  //   BSPAN == 2: iteration i issues A(i+1), then on even i B stage i/2+1;
+  //     after A(kt+1) comes that B stage when kt is even (B stage (kt+1)/2,
+  //     needed when kt is odd, was issued before A(kt)).
+  // kt = -1 is the prologue's wait for tile 0 (same issue order there).
+  static __device__ __forceinline__ void wait_next(int kt, int nk) {
+    const int rem = nk - 1 - kt;  // K tiles from kt+1 on
+    if constexpr (BSPAN == 2) {
+      if (kt >= 0 && (kt & 1) == 0 && kt + 2 < nk) wait_vmcnt<B_INST>();
+      else wait_vmcnt<0>();
+    } else if constexpr (SA == SB) {
+      if (SB > 3 && rem >= 3) wait_vmcnt<(SB > 3 ? 2 * INST : 0)>();
+      else if (SB > 2 && rem >= 2) wait_vmcnt<(SB > 2 ? INST : 0)>();
+      else wait_vmcnt<0>();
+    } else {
+      if (SA == 3 && rem >= 3) wait_vmcnt<(SA == 3 ? INST + B_INST : 0)>();
+      else if (SA == 3 && rem >= 2) wait_vmcnt<(SA == 3 ? INST : 0)>();
+      else if (rem >= 2) wait_vmcnt<B_INST>();
+      else wait_vmcnt<0>();
+    }
   }
 
-  // Software pipeline over K tiles (tile kt lives in stage kt % STAGES):
-  //   k-step 0 of tile kt: its MFMAs interleaved with the DMA of tile
-  //     kt+STAGES-1 (into the stage tile kt-1 used, released by the previous
-  //     barrier) and the fragment reads of the next k-step;
-  //   last k-step: half the MFMAs, then the tile boundary (wait for tile
-  //     kt+1, barrier, first fragments of tile kt+1), then the other half.
-  // The barrier also certifies that every wave finished reading tile kt, so
-  // its stage may be refilled during tile kt+1.
-  // fp8: MFMAs accumulate the current 128-wide K block in `mac`, which is
-  // scaled by the block's scale (per N block, sc[j] + kb) and added to `acc`.
-  // One K tile (see run()).  FRESH: the tile starts an fp8 scale block, so its
-  // first k-step overwrites the partial sums instead of accumulating.
+  // One K tile.  k-step 0: its MFMAs interleaved with the DMA of A tile
+  // kt+SA-1 and B tile kt+SB-1 (into the stages tile kt-1 used, released by
+  // the previous barrier) and the fragment reads of the next k-step.  Last
+  // k-step: half the MFMAs, then the tile boundary (wait for tile kt+1,
+  // barrier, first fragments of tile kt+1), then the other half.  The barrier
+  // also certifies that every wave finished reading tile kt, so its stages
+  // may be refilled during tile kt+1.  FRESH: the tile starts an fp8 scale
+  // block, so its first k-step overwrites the partial sums.
   template <bool FRESH>
   static __device__ __forceinline__ void tile(const LDS_AS char* smem, const Src& s, int nk,
                                               int kt, int a_lane_off,
@@ -421,25 +461,28 @@ struct DmaLoop {
                                               f32x16 (&mac)[MBW][NBW]) {
     const int khalf = (threadIdx.x & 63) >> 5;
     auto coff = [&](int kk) { return (((2 * kk + khalf) ^ s_l) << 4); };
-    const LDS_AS char* src = smem + (kt % STAGES) * STAGE_BYTES;
-    const int nx = kt + STAGES - 1;
-    const bool refill = nx < nk;
-    const uint32_t dst = s.lds + (nx % STAGES) * STAGE_BYTES;
+    const LDS_AS char* asrc = smem + (kt % SA) * A_BYTES;
+    const LDS_AS char* bsrc = smem + B_BASE + ((kt / BSPAN) % SB) * B_BYTES;
+    const int kp = kt % BSPAN;
+    const int nb = (nk + BSPAN - 1) / BSPAN;
+    const int ka = kt + SA - 1;
+    const int kb = kp == 0 ? kt / BSPAN + SB - 1 : -1;  // B stages start on even tiles
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       Frags& fa = f[kk & 1];
       Frags& fb = f[(kk + 1) & 1];
       if (kk + 1 < KK) {
-        load_b(src, kk + 1, coff(kk + 1), b_lane_off, sb_l, fb);
+        load_b(bsrc, kk + 1, kp, coff(kk + 1), b_lane_off, sb_l, fb);
 #pragma unroll
         for (int i = 0; i < MBW; ++i) {
-          load_a(src, coff(kk + 1), i, a_lane_off, mb_live, fb);
+          load_a(asrc, coff(kk + 1), i, a_lane_off, mb_live, fb);
           if (FRESH && kk == 0) mma_row<true>(fa, i, mb_live, mac);
           else mma_row(fa, i, mb_live, mac);
-          if (kk == 0 && refill) {
+          if (kk == 0) {
             // spread the INST DMA instructions over the MBW row blocks
 #pragma unroll
-            for (int q = i * INST / MBW; q < (i + 1) * INST / MBW; ++q) issue_one(s, dst, nx, q);
+            for (int q = i * INST / MBW; q < (i + 1) * INST / MBW; ++q)
+              issue_one(s, ka, kb, nk, nb, q);
           }
         }
       } else {
@@ -447,12 +490,13 @@ struct DmaLoop {
         for (int i = 0; i < MBW / 2; ++i) mma_row(fa, i, mb_live, mac);
         if (kt + 1 < nk) {
           asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-          wait_tiles(min(STAGES - 2, nk - 2 - kt));
+          wait_next(kt, nk);
           lds_barrier();
-          const LDS_AS char* nsrc = smem + ((kt + 1) % STAGES) * STAGE_BYTES;
-          load_b(nsrc, 0, coff(0), b_lane_off, sb_l, fb);
+          const LDS_AS char* nasrc = smem + ((kt + 1) % SA) * A_BYTES;
+          const LDS_AS char* nbsrc = smem + B_BASE + (((kt + 1) / BSPAN) % SB) * B_BYTES;
+          load_b(nbsrc, 0, (kt + 1) % BSPAN, coff(0), b_lane_off, sb_l, fb);
 #pragma unroll
-          for (int i = 0; i < MBW; ++i) load_a(nsrc, coff(0), i, a_lane_off, mb_live, fb);
+          for (int i = 0; i < MBW; ++i) load_a(nasrc, coff(0), i, a_lane_off, mb_live, fb);
         }
 #pragma unroll
         for (int i = MBW / 2; i < MBW; ++i) mma_row(fa, i, mb_live, mac);
@@ -460,48 +504,61 @@ struct DmaLoop {
     }
   }
 
-  // Software pipeline over K tiles (tile kt lives in stage kt % STAGES):
-  //   k-step 0 of tile kt: its MFMAs interleaved with the DMA of tile
-  //     kt+STAGES-1 (into the stage tile kt-1 used, released by the previous
-  //     barrier) and the fragment reads of the next k-step;
-  //   last k-step: half the MFMAs, then the tile boundary (wait for tile
-  //     kt+1, barrier, first fragments of tile kt+1), then the other half.
-  // The barrier also certifies that every wave finished reading tile kt, so
-  // its stage may be refilled during tile kt+1.
+  // Prologue (in the issue order wait_next assumes), then the K tiles.
   // fp8: the MFMAs of one 128-wide K block (TILES_PER_SCALE tiles) go to
   // `part`, which is then scaled by the block's scale (per N block,
   // sc[j][kb]) and added to `acc`.
   static __device__ __forceinline__ void run(const LDS_AS char* smem, const Src& s, int nk,
                                              int a_lane_off, const int (&b_lane_off)[NBW],
                                              int s_l, int sb_l, int mb_live,
-                                             const float* const (&sc)[NBW],
+                                             const CONST_AS float* const (&sc)[NBW],
                                              f32x16 (&acc)[MBW][NBW]) {
     const int khalf = (threadIdx.x & 63) >> 5;
     const int coff0 = ((khalf ^ s_l) << 4);
+    const int nb = (nk + BSPAN - 1) / BSPAN;
+    if constexpr (BSPAN == 2) {
+      issue_b(s, 0, nb);
+      issue_a(s, 0, nk);
+    } else if constexpr (SA == SB) {
 #pragma unroll
-    for (int t = 0; t < STAGES - 1; ++t)
-      if (t < nk) issue(s, s.lds + t * STAGE_BYTES, t);
-    wait_tiles(min(STAGES - 2, nk - 1));
+      for (int t = 0; t < SA - 1; ++t) {
+        issue_a(s, t, nk);
+        issue_b(s, t, nb);
+      }
+    } else {
+      issue_b(s, 0, nb);
+#pragma unroll
+      for (int t = 0; t < SA - 1; ++t) {
+        issue_a(s, t, nk);
+        issue_b(s, t + 1, nb);
+      }
+    }
+    wait_next(-1, nk);
     lds_barrier();
     Frags f[2];
-    load_b(smem, 0, coff0, b_lane_off, sb_l, f[0]);
+    load_b(smem + B_BASE, 0, 0, coff0, b_lane_off, sb_l, f[0]);
 #pragma unroll
     for (int i = 0; i < MBW; ++i) load_a(smem, coff0, i, a_lane_off, mb_live, f[0]);
 
     if constexpr (FP8) {
       f32x16 part[MBW][NBW];
       for (int kt = 0; kt < nk; kt += TILES_PER_SCALE) {
+        // the block's scales come through the scalar cache (lgkmcnt), issued
+        // before its MFMAs: a vector load here would make the compiler wait
+        // for vmcnt(0), draining the DMA ring it does not know about
+        const int kb = kt / TILES_PER_SCALE;
+        float scale[NBW];
+#pragma unroll
+        for (int j = 0; j < NBW; ++j) scale[j] = sc[j][kb];
         tile<true>(smem, s, nk, kt, a_lane_off, b_lane_off, s_l, sb_l, mb_live, f, part);
 #pragma unroll
         for (int u = 1; u < TILES_PER_SCALE; ++u)
           tile<false>(smem, s, nk, kt + u, a_lane_off, b_lane_off, s_l, sb_l, mb_live, f, part);
-        const int kb = kt / TILES_PER_SCALE;
 #pragma unroll
         for (int j = 0; j < NBW; ++j) {
-          const float scale = sc[j][kb];
 #pragma unroll
           for (int i = 0; i < MBW; ++i)
-            if (FULL || i < mb_live) acc[i][j] += scale * part[i][j];
+            if (FULL || i < mb_live) acc[i][j] += scale[j] * part[i][j];
         }
       }
     } else {
@@ -511,7 +568,7 @@ struct DmaLoop {
   }
 };
 
-template <int KIND, bool FP8, int BK, int STAGES, int WM, int WN, int MBW, int NBW>
+template <int KIND, bool FP8, int BK, int SA, int SB, int BSPAN, int WM, int WN, int MBW, int NBW>
 __global__ __launch_bounds__(WM * WN * kWave)
 __attribute__((amdgpu_waves_per_eu(WM * WN / 4, WM * WN / 4)))
 void grouped_gemm_dma_kernel(GemmParams p) {
@@ -520,18 +577,23 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   constexpr int BM = WM * MBW * 32, BN = WN * NBW * 32;
   constexpr bool GATEUP = KIND == kGateUp;
   static_assert(!GATEUP || (NBW % 2 == 0), "gate/up pairs gate and up blocks");
-  using Full = DmaLoop<KIND, BK, STAGES, NW, BM, BN, MBW, NBW, true, FP8>;
-  using Part = DmaLoop<KIND, BK, STAGES, NW, BM, BN, MBW, NBW, false, FP8>;
+  using Full = DmaLoop<KIND, BK, SA, SB, BSPAN, NW, BM, BN, MBW, NBW, true, FP8>;
+  using Part = DmaLoop<KIND, BK, SA, SB, BSPAN, NW, BM, BN, MBW, NBW, false, FP8>;
   constexpr int RB = Full::RB, CH = Full::CH, RPI = Full::RPI;
   constexpr int BRB = Full::BRB, BCH = Full::BCH, BRPI = Full::BRPI;
 
-  __shared__ __attribute__((aligned(1024))) char smem_raw[STAGES * Full::STAGE_BYTES];
-  __shared__ int s_tp[kMaxExperts + 1];
-  __shared__ int s_exp[kMaxExperts];
+  // the scheduler's tables live in the stage memory until the tile is located
+  static_assert(Full::LDS_BYTES >= (2 * kMaxExperts + 1) * 4, "scheduler tables");
+  __shared__ __attribute__((aligned(1024))) char smem_raw[Full::LDS_BYTES];
   __shared__ int s_wave[NT / kWave + 1];
 
   Tile t;
-  if (!locate_tile<BM, BN, NT>(p, s_tp, s_exp, s_wave, t)) return;
+  {
+    int* s_tp = reinterpret_cast<int*>(smem_raw);
+    int* s_exp = s_tp + kMaxExperts + 1;
+    if (!locate_tile<BM, BN, NT>(p, s_tp, s_exp, s_wave, t)) return;
+    __syncthreads();  // every lane has its tile before the DMA overwrites the tables
+  }
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
@@ -549,7 +611,7 @@ void grouped_gemm_dma_kernel(GemmParams p) {
       const int row = Full::a_inst(wave, i) * RPI + drow;
       const int r = t.r0 + (row < t.rows_valid ? row : 0);
       const int src_row = GATEUP ? min(max(p.perm[r], 0), p.R - 1) / p.k : r;
-      src.a_off[i] = (uint32_t)(src_row * p.lda + ((dpc ^ swz<BK>(row)) * 8)) * 2u;
+      src.a_off[i] = (uint32_t)(src_row * p.lda + ((dpc ^ swz<RB>(row)) * 8)) * 2u;
     }
   }
   {
@@ -558,7 +620,7 @@ void grouped_gemm_dma_kernel(GemmParams p) {
 #pragma unroll
     for (int i = 0; i < Full::B_INST; ++i) {
       const int j = Full::b_inst(wave, i) * BRPI + drow;
-      const int chunk = dpc ^ (FP8 ? swz<32>(j) : swz<BK>(j));
+      const int chunk = dpc ^ swz<BRB>(j);
       src.b_off[i] = (uint32_t)weight_row<GATEUP, BN>(p, t.tn, j) * (uint32_t)p.K * (FP8 ? 1u : 2u) +
                      (uint32_t)chunk * 16u;
     }
@@ -570,17 +632,18 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   const int am0 = wm * MBW * 32;
   const int a_lane_off = (am0 + lrow) * RB;
   int b_lane_off[NBW];
-  const float* sc[NBW];
+  const CONST_AS float* sc[NBW];  // per N block: its row of 128x128 scales (wave-uniform)
 #pragma unroll
   for (int j = 0; j < NBW; ++j) {
     const int br = block_row<GATEUP, BN, NBW>(wn, j);
     b_lane_off[j] = (br + lrow) * BRB;
-    sc[j] = FP8 ? p.b_scale + ((size_t)t.e * (p.N / 128) + weight_row<GATEUP, BN>(p, t.tn, br) / 128) *
-                                  (p.K / 128)
+    sc[j] = FP8 ? (const CONST_AS float*)wave_uniform(
+                      p.b_scale + ((size_t)t.e * (p.N / 128) +
+                                   weight_row<GATEUP, BN>(p, t.tn, br) / 128) * (p.K / 128))
                 : nullptr;
   }
-  const int s_l = swz<BK>(lrow);
-  const int sb_l = swz<32>(lrow);
+  const int s_l = swz<RB>(lrow);
+  const int sb_l = swz<BRB>(lrow);
   const int mb_live =
       __builtin_amdgcn_readfirstlane(max(0, min(MBW, ceil_div(t.rows_valid - am0, 32))));
 
@@ -797,13 +860,13 @@ hipError_t launch_reg(const GemmParams& p, int R, int E, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int KIND, bool FP8, int BK, int STAGES, int WM, int WN, int MBW, int NBW>
+template <int KIND, bool FP8, int BK, int SA, int SB, int BSPAN, int WM, int WN, int MBW, int NBW>
 hipError_t launch_dma(const GemmParams& p, int R, int E, hipStream_t stream) {
   constexpr int BM = WM * MBW * 32, BN = WN * NBW * 32;
   const long long grid = grid_tiles(R, E, BM, BN, p.N);
   if (grid <= 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((grouped_gemm_dma_kernel<KIND, FP8, BK, STAGES, WM, WN, MBW, NBW>),
+  hipLaunchKernelGGL((grouped_gemm_dma_kernel<KIND, FP8, BK, SA, SB, BSPAN, WM, WN, MBW, NBW>),
                      dim3((unsigned)grid), dim3(WM * WN * kWave), 0, stream, p);
   return hipGetLastError();
 }
@@ -821,8 +884,8 @@ template <int KIND, bool FP8>
 hipError_t launch_kind(const GemmParams& p, int R, int E, bool small_m, hipStream_t stream) {
   const bool n256 = (p.N % 256) == 0;
   if constexpr (FP8) {
-    if (p.N % 512 == 0) return launch_dma<KIND, true, 64, 3, 1, 8, 3, 2>(p, R, E, stream);
-    if (n256) return launch_dma<KIND, true, 64, 3, 1, 4, 3, 2>(p, R, E, stream);
+    if (p.N % 512 == 0) return launch_dma<KIND, true, 64, 3, 3, 1, 1, 8, 3, 2>(p, R, E, stream);
+    if (n256) return launch_dma<KIND, true, 64, 3, 3, 1, 1, 4, 3, 2>(p, R, E, stream);
     if (small_m) return launch_reg<KIND, true, 1, 2, 4, 2>(p, R, E, stream);
     return launch_reg<KIND, true, 2, 2, 4, 2>(p, R, E, stream);
   } else {
@@ -830,7 +893,7 @@ hipError_t launch_kind(const GemmParams& p, int R, int E, bool small_m, hipStrea
       if (n256) return launch_reg<KIND, false, 1, 4, 4, 2>(p, R, E, stream);
       return launch_reg<KIND, false, 1, 2, 4, 2>(p, R, E, stream);
     }
-    if (n256) return launch_dma<KIND, false, 64, 2, 2, 4, 4, 2>(p, R, E, stream);
+    if (n256) return launch_dma<KIND, false, 64, 2, 2, 1, 2, 4, 4, 2>(p, R, E, stream);
     return launch_reg<KIND, false, 2, 2, 4, 2>(p, R, E, stream);
   }
 }
