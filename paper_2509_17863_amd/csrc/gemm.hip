@@ -15,16 +15,16 @@
 // gate rows followed by the matching BN/2 up rows, and each wave's blocks pair
 // a gate block with the up block of the same columns.
 //
-// Two main loops:
-//   * bf16 weights: operands go global -> LDS directly (global_load_lds, 16 B
-//     per lane, no VGPR staging) through a ring of STAGES buffers; tile kt+S-1
-//     is in flight while tile kt is multiplied.  Waits are explicit vmcnt
-//     counts plus a bare s_barrier.
-//   * fp8-e4m3 weights (one fp32 scale per 128x128 block): operands go global
-//     -> VGPR -> LDS (double buffered) so the weights can be converted to bf16
-//     on the way (exact); each 128-wide K block's MFMA partial sum is scaled
-//     and added to the fp32 accumulator.
-// LDS rows are BK bf16 long; 16-byte chunk c of row r is stored at chunk
+// Main loop (bf16 and fp8 weights alike): operands go global -> LDS directly
+// (global_load_lds, 16 B per lane, no VGPR staging) through a ring of SA
+// token-row stages and SB weight stages; the next tiles are in flight while
+// tile kt is multiplied.  Waits are explicit vmcnt counts plus a bare
+// s_barrier.  fp8-e4m3 weights (one fp32 scale per 128x128 block) stay fp8 in
+// LDS and are converted to bf16 (exactly) as fragments are read; each
+// 128-wide K block's MFMA partial sum is scaled and added to the fp32
+// accumulator.  A register-staged loop covers shapes the DMA tiles do not
+// (N not a multiple of 256, decode-sized bf16 batches).
+// LDS rows are BK elements long; 16-byte chunk c of row r is stored at chunk
 // c ^ swz(r) so 32-row fragment reads hit every bank once.
 //
 // Scheduling: the workgroup reads the compacted active list (group-shrink)
