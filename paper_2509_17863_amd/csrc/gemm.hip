@@ -15,15 +15,19 @@
 // gate rows followed by the matching BN/2 up rows, and each wave's blocks pair
 // a gate block with the up block of the same columns.
 //
-// Main loop (bf16 and fp8 weights alike): operands go global -> LDS directly
-// (global_load_lds, 16 B per lane, no VGPR staging) through a ring of SA
-// token-row stages and SB weight stages; the next tiles are in flight while
-// tile kt is multiplied.  Waits are explicit vmcnt counts plus a bare
-// s_barrier.  fp8-e4m3 weights (one fp32 scale per 128x128 block) stay fp8 in
-// LDS and are converted to bf16 (exactly) as fragments are read; each
-// 128-wide K block's MFMA partial sum is scaled and added to the fp32
-// accumulator.  A register-staged loop covers shapes the DMA tiles do not
-// (N not a multiple of 256, decode-sized bf16 batches).
+// Operands go global -> LDS directly (global_load_lds, 16 B per lane, no VGPR
+// staging) through rings of token-row (A) and weight (B) stages; later tiles
+// are in flight while one is multiplied.  Waits are explicit vmcnt counts plus
+// a bare s_barrier.  Two main loops use this:
+//   - bf16 weights, prefill-sized batches: an 8-wave ping-pong in which the
+//     two waves of each SIMD alternate between reading a whole K tile's
+//     fragments from LDS and issuing its MFMAs (grouped_gemm_pp_kernel);
+//   - fp8-e4m3 weights (one fp32 scale per 128x128 block): the weights stay
+//     fp8 in LDS and are converted to bf16 (exactly) as fragments are read;
+//     each 128-wide K block's MFMA partial sum is scaled and added to the
+//     fp32 accumulator (grouped_gemm_dma_kernel).
+// A register-staged loop covers shapes the DMA tiles do not (N not a multiple
+// of 256, decode-sized bf16 batches).
 // LDS rows are BK elements long; 16-byte chunk c of row r is stored at chunk
 // c ^ swz(r) so 32-row fragment reads hit every bank once.
 //
@@ -34,6 +38,8 @@
 // tiles; workgroup ids are remapped so each XCD (ids congruent mod 8) gets a
 // contiguous range of tiles and its L2 sees that reuse.  The grid is sized for the worst case from R and E alone (no
 // host readback); surplus workgroups exit after the prologue.
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 
@@ -871,8 +877,216 @@ hipError_t launch_dma(const GemmParams& p, int R, int E, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// ============================================================================
+// bf16 weights, prefill-sized batches: 8-wave ping-pong
+// ============================================================================
+// 256x256 tiles, BK = 64, 8 waves in two groups of four (one wave of each
+// group per SIMD).  Group 0 owns token rows 0-127 of the tile and group 1
+// rows 128-255; inside a group wave w4 owns a 64-column slice (two 32-column
+// blocks; for gate/up a gate block and the up block of the same columns).
+// The groups walk the same K tiles one phase apart.  In an M phase a wave
+// issues its share of the operand DMA and reads all four k-steps of its
+// fragments of one K tile from LDS into registers; in a C phase it issues
+// the 32 MFMAs of those fragments.  While one group multiplies, the other
+// reads, so each SIMD's matrix pipe is fed by one of its two waves at a
+// time and the LDS reads stay off the MFMA issue path.  Every phase ends
+// with an s_barrier of all eight waves:
+//   group 0, phase 2t:   M(t): DMA of A tile t+1 (t >= 1), fragments of tile t
+//   group 0, phase 2t+1: C(t), then wait until A tile t+1 has landed
+//   group 1, phase 2t+1: M(t): DMA of B tile t+2, fragments of tile t, wait
+//                        until B tile t+1 has landed
+//   group 1, phase 2t+2: C(t)
+// A (token rows) has 2 LDS stages and B (weight rows, streamed from HBM) 3.
+// A stage is refilled only in the phase after both groups have read it, and
+// each tile lands by the barrier before group 0 reads it (A one phase after
+// its DMA was issued, B three).  The MFMA order per accumulator is the same
+// as in the other GEMM loops: k-steps ascending within a tile, tiles
+// ascending, so results do not depend on which loop ran.
+template <int KIND>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void grouped_gemm_pp_kernel(GemmParams p) {
+  constexpr int BM = 256, BN = 256, BK = 64, MBW = 4, NBW = 2, NT = 512;
+  constexpr int RB = BK * 2;   // bytes per LDS row (A and B)
+  constexpr int KK = BK / 16;  // MFMA k-steps per K tile
+  constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB;
+  constexpr int SA = 2, SB = 3;
+  constexpr int B_BASE = SA * A_BYTES;
+  constexpr int LDS_BYTES = SA * A_BYTES + SB * B_BYTES;  // 160 KiB
+  constexpr int INST = 8;      // DMA instructions of one wave per K tile of its operand
+  constexpr bool GATEUP = KIND == kGateUp;
+  static_assert(INST * 4 * 8 == BM && BM == BN, "4 waves x INST instructions x 8 rows");
+  static_assert(LDS_BYTES >= (2 * kMaxExperts + 2 + NT / kWave) * 4, "scheduler tables");
+  __shared__ __attribute__((aligned(1024))) char smem_raw[LDS_BYTES];
+
+  Tile t;
+  {
+    // the scheduler's tables live in the stage memory until the tile is located
+    int* s_tp = reinterpret_cast<int*>(smem_raw);
+    int* s_exp = s_tp + kMaxExperts + 1;
+    int* s_wave = s_exp + kMaxExperts + 1;
+    if (!locate_tile<BM, BN, NT>(p, s_tp, s_exp, s_wave, t)) return;
+    __syncthreads();  // every lane has its tile before the DMA overwrites the tables
+  }
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  const int grp = wave >> 2;  // 0: rows 0-127, streams A; 1: rows 128-255, streams B
+  const int w4 = wave & 3;
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem_raw);
+
+  // DMA: instruction q of this wave moves rows (w4 + 4q)*8 .. +8 of its
+  // group's operand; lane l writes 16 bytes at (row l/8, physical chunk l%8),
+  // so it fetches logical chunk (l%8) ^ swizzle(row)
+  const char* dbase;
+  uint32_t doff[INST];
+  {
+    const int drow = lane >> 3, dpc = lane & 7;
+    if (grp == 0) {
+      dbase = reinterpret_cast<const char*>(p.a);
+#pragma unroll
+      for (int q = 0; q < INST; ++q) {
+        const int row = (w4 + 4 * q) * 8 + drow;
+        const int r = t.r0 + (row < t.rows_valid ? row : 0);
+        const int src_row = GATEUP ? min(max(p.perm[r], 0), p.R - 1) / p.k : r;
+        doff[q] = (uint32_t)(src_row * p.lda + ((dpc ^ swz<RB>(row)) * 8)) * 2u;
+      }
+    } else {
+      dbase = reinterpret_cast<const char*>(p.b) + (size_t)t.e * p.N * p.K * 2;
+#pragma unroll
+      for (int q = 0; q < INST; ++q) {
+        const int j = (w4 + 4 * q) * 8 + drow;
+        doff[q] = (uint32_t)weight_row<GATEUP, BN>(p, t.tn, j) * (uint32_t)p.K * 2u +
+                  (uint32_t)((dpc ^ swz<RB>(j)) * 16);
+      }
+    }
+  }
+  // DMA of K tile kt of this wave's operand into its ring slot
+  auto issue = [&](int kt) {
+    const char* src = dbase + kt * BK * 2;
+    const uint32_t dst = grp == 0 ? lds0 + (kt % SA) * A_BYTES + w4 * 8 * RB
+                                  : lds0 + B_BASE + (kt % SB) * B_BYTES + w4 * 8 * RB;
+#pragma unroll
+    for (int q = 0; q < INST; ++q) dma16(src, doff[q], dst + q * 4 * 8 * RB);
+  };
+
+  const int wn = w4;
+  const int lrow = lane & 31;
+  const int khalf = lane >> 5;
+  const int am0 = grp * MBW * 32;
+  const int a_lane_off = (am0 + lrow) * RB;
+  int b_lane_off[NBW];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) b_lane_off[j] = (block_row<GATEUP, BN, NBW>(wn, j) + lrow) * RB;
+  const int s_l = swz<RB>(lrow);  // rows am0 + 32i + lrow share lrow's swizzle
+  const int mb_live =
+      __builtin_amdgcn_readfirstlane(max(0, min(MBW, ceil_div(t.rows_valid - am0, 32))));
+
+  f32x16 acc[MBW][NBW];
+#pragma unroll
+  for (int i = 0; i < MBW; ++i)
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) acc[i][j] = f32x16{};
+  const LDS_AS char* smem = (const LDS_AS char*)smem_raw;
+  const int nk = p.K / BK;
+
+  auto phase_end = [&]() {
+    // keep the scheduler from moving MFMAs or LDS reads across the barrier
+    __builtin_amdgcn_sched_barrier(0);
+    lds_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // FULL: every row block of the tile holds rows (no per-block checks)
+  auto main_loop = [&](auto full) {
+    constexpr bool FULL = decltype(full)::value;
+    bf16x8 fa[KK][MBW];
+    bf16x8 fb[KK][NBW];
+    auto load_frags = [&](int kt) {
+      const LDS_AS char* asrc = smem + (kt % SA) * A_BYTES;
+      const LDS_AS char* bsrc = smem + B_BASE + (kt % SB) * B_BYTES;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const int coff = ((2 * kk + khalf) ^ s_l) << 4;
+#pragma unroll
+        for (int j = 0; j < NBW; ++j)
+          fb[kk][j] = *reinterpret_cast<const LDS_AS bf16x8*>(bsrc + b_lane_off[j] + coff);
+#pragma unroll
+        for (int i = 0; i < MBW; ++i)
+          if (FULL || i < mb_live)
+            fa[kk][i] =
+                *reinterpret_cast<const LDS_AS bf16x8*>(asrc + a_lane_off + i * 32 * RB + coff);
+      }
+      // the stage may be refilled right after the next barrier
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    };
+    auto mfmas = [&]() {
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+        for (int i = 0; i < MBW; ++i)
+          if (FULL || i < mb_live)
+#pragma unroll
+            for (int j = 0; j < NBW; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[kk][j], fa[kk][i],
+                                                                  acc[i][j], 0, 0, 0);
+    };
+
+    // prologue: each group's first two K tiles of its operand; tile 0 must
+    // have landed before the first barrier
+    issue(0);
+    if (nk > 1) {
+      issue(1);
+      wait_vmcnt<INST>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    phase_end();
+    // both groups pass 2*nk + 1 phase barriers: group 1 idles in the first
+    // phase, group 0 in the last
+    if (grp == 0) {
+      for (int kt = 0; kt < nk; ++kt) {
+        if (kt >= 1 && kt + 1 < nk) issue(kt + 1);
+        load_frags(kt);
+        phase_end();
+        mfmas();
+        wait_vmcnt<0>();  // A tile kt+1 (issued in the previous phase) has landed
+        phase_end();
+      }
+      phase_end();
+    } else {
+      phase_end();
+      for (int kt = 0; kt < nk; ++kt) {
+        if (kt + 2 < nk) issue(kt + 2);
+        load_frags(kt);
+        // B tile kt+1 has landed; B tile kt+2 may still be in flight
+        if (kt + 2 < nk) wait_vmcnt<INST>();
+        else wait_vmcnt<0>();
+        phase_end();
+        mfmas();
+        phase_end();
+      }
+    }
+  };
+  if (t.rows_valid == BM) main_loop(std::true_type{});
+  else main_loop(std::false_type{});
+
+  // the epilogue's row information is loaded only now: a vector load in
+  // the loop would make the compiler wait for vmcnt(0) there
+  const RowInfo<MBW> ri = row_info<KIND, MBW>(p, t, am0, mb_live);
+  epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, ri, acc);
+}
+
+template <int KIND>
+hipError_t launch_pp(const GemmParams& p, int R, int E, hipStream_t stream) {
+  const long long grid = grid_tiles(R, E, 256, 256, p.N);
+  if (grid <= 0) return hipSuccess;
+  if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((grouped_gemm_pp_kernel<KIND>), dim3((unsigned)grid), dim3(512), 0, stream,
+                     p);
+  return hipGetLastError();
+}
+
 // Tile shapes (N a multiple of 256 takes the LDS-DMA kernels):
-//   bf16, prefill-sized: 256x256 tiles, 8 waves of 128x64, BK=64, 2 stages;
+//   bf16, prefill-sized: 256x256 tiles, 8 waves of 128x64 in ping-pong, BK=64;
 //   fp8 weights: 96x512 tiles (a decode batch's ~50-90 rows per expert fit
 //     one tile, so the weights stream once), 8 waves of 96x64 -- two per
 //     SIMD, so one wave's partial-sum scaling (VALU) overlaps the other's
@@ -893,7 +1107,7 @@ hipError_t launch_kind(const GemmParams& p, int R, int E, bool small_m, hipStrea
       if (n256) return launch_reg<KIND, false, 1, 4, 4, 2>(p, R, E, stream);
       return launch_reg<KIND, false, 1, 2, 4, 2>(p, R, E, stream);
     }
-    if (n256) return launch_dma<KIND, false, 64, 2, 2, 1, 2, 4, 4, 2>(p, R, E, stream);
+    if (n256) return launch_pp<KIND>(p, R, E, stream);
     return launch_reg<KIND, false, 2, 2, 4, 2>(p, R, E, stream);
   }
 }
