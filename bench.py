@@ -44,6 +44,16 @@ def algorithmic(d: dict, counts: np.ndarray) -> dict:
                 bytes=gu_bytes + dn_bytes - R * I * 2 * 0 + T * k * 4)
 
 
+def gate_up_kernel_name(d: dict) -> str:
+    """The gate/up kernel the library dispatches for this workload's shape."""
+    T, I, E, k = d["T"], d["I"], d["E"], d["k"]
+    if d["wdtype"] == "fp8":
+        return "grouped_gemm_dma_kernel<gate/up, fp8 weights>"
+    if T * k <= 128 * E or (2 * I) % 256:
+        return "grouped_gemm_kernel<gate/up, register-staged>"
+    return "grouped_gemm_pp_kernel<gate/up>"
+
+
 def kernel_source_sha256() -> str:
     h = hashlib.sha256()
     for f in ("gemm.hip", "common.h", "internal.h"):
@@ -174,7 +184,7 @@ def main() -> int:
     roof["traffic"] = measured_traffic(args.workload)
     roof["traffic_unit"] = "bytes per launch"
     roof["algorithmic_bytes"] = int(alg["gu_bytes"])
-    roof["kernel"] = "grouped_gemm_dma_kernel<gate/up>"
+    roof["kernel"] = gate_up_kernel_name(d)
     res = {
         "metric": "expert-FFN tokens/s",
         "value": round(T / (ms * 1e-3), 1),
