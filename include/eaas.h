@@ -169,6 +169,56 @@ int eaas_expert_forward_profiled(const eaas_shape *s, const void *x,
                                  size_t ws_bytes, void *stream,
                                  void *const *events);
 
+/*
+ * Dynamic batch of several clients' requests (§3.3: the server aggregates the
+ * ready requests of its clients into one batch and writes each client's
+ * results back into that client's payload; §3.2: a buffer slot's payload and
+ * its header's batch size).
+ *
+ * One request, as laid out in a client's buffer slot (device pointers,
+ * 16-byte aligned; only the first num_tokens[b] rows belong to the request):
+ *   x            [n,H] bf16 hidden states
+ *   topk_ids     [n,k] int32 expert ids (ids outside [0,E) are skipped)
+ *   topk_weights [n,k] fp32 router scores
+ *   out          [n,H] weighted sums, bf16 or fp32 per out_dtype.  out == x
+ *                (bf16) writes the result back into the payload in place; out
+ *                must not overlap any other request's arrays.
+ */
+typedef struct eaas_segment {
+  const void *x;
+  const int32_t *topk_ids;
+  const float *topk_weights;
+  void *out;
+} eaas_segment;
+
+/* Workspace bytes of eaas_expert_forward_segments for a capacity of s->T
+ * tokens (0 for a shape the library rejects). */
+size_t eaas_segments_workspace_bytes(const eaas_shape *s, int w_dtype);
+
+/* The step on a dynamic batch of requests whose token counts are read on the
+ * device, so the same call (or a captured graph of it) serves any mix of
+ * batch sizes.  The tokens are walked with Algorithm 1 of §4 (a static grid
+ * over requests of varying length that skips empty ones).
+ *   s->T        capacity: grids and workspace are sized for at most s->T
+ *               tokens in all requests together
+ *   segs        [n_seg] eaas_segment, a DEVICE array
+ *   num_tokens  [n_seg] int32, a DEVICE array: request b's batch size (header
+ *               batch_size).  0 means no request from that client this step;
+ *               negative counts count as 0.  Requests are batched in slot
+ *               order; tokens past the capacity are not processed and their
+ *               out rows are left untouched.
+ *   n_seg       0..1024 (0: nothing enqueued)
+ * For every request b, out rows [0, num_tokens[b]) receive exactly what
+ * eaas_expert_forward writes for those tokens when run on the requests
+ * concatenated in slot order; no other memory of the requests is written. */
+int eaas_expert_forward_segments(const eaas_shape *s, const eaas_segment *segs,
+                                 const int32_t *num_tokens, int n_seg,
+                                 const void *w_gate_up,
+                                 const float *w_gate_up_scale,
+                                 const void *w_down, const float *w_down_scale,
+                                 int w_dtype, int out_dtype, void *ws,
+                                 size_t ws_bytes, void *stream);
+
 /* Static, human-readable name of a status code. */
 const char *eaas_status_string(int status);
 

@@ -17,6 +17,8 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 struct WsLayout {
   size_t hist, counts, offsets, perm, inv, active, h, stage, total;
+  // dynamic batch only: the requests gathered into one contiguous batch
+  size_t x_cat, ids_cat, w_cat, seg_total;
 };
 
 WsLayout layout(const eaas_shape& s) {
@@ -32,6 +34,10 @@ WsLayout layout(const eaas_shape& s) {
   L.h = o;       o = align_up(o + R * s.I * 2);
   L.stage = o;   o = align_up(o + R * s.H * 4);
   L.total = o;
+  L.x_cat = o;   o = align_up(o + (size_t)s.T * s.H * 2);
+  L.ids_cat = o; o = align_up(o + R * 4);
+  L.w_cat = o;   o = align_up(o + R * 4);
+  L.seg_total = o;
   return L;
 }
 
@@ -214,6 +220,63 @@ int eaas_expert_forward(const eaas_shape* s, const void* x, const int32_t* topk_
   return eaas_expert_forward_profiled(s, x, topk_ids, topk_weights, w_gate_up, w_gate_up_scale,
                                       w_down, w_down_scale, w_dtype, out, out_dtype, r, ws,
                                       ws_bytes, stream, nullptr);
+}
+
+size_t eaas_segments_workspace_bytes(const eaas_shape* s, int w_dtype) {
+  if (check_shape(s) != EAAS_OK) return 0;
+  if (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3) return 0;
+  return layout(*s).seg_total;
+}
+
+int eaas_expert_forward_segments(const eaas_shape* s, const eaas_segment* segs,
+                                 const int32_t* num_tokens, int n_seg, const void* w_gate_up,
+                                 const float* w_gate_up_scale, const void* w_down,
+                                 const float* w_down_scale, int w_dtype, int out_dtype, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  int st = check_shape(s);
+  if (st != EAAS_OK) return st;
+  if (n_seg < 0 || n_seg > kMaxSegments) return EAAS_ERR_INVALID_ARG;
+  if (s->T == 0 || n_seg == 0) return EAAS_OK;
+  if (!segs || !num_tokens || (out_dtype != EAAS_BF16 && out_dtype != EAAS_FP32) ||
+      !weights_ok(w_gate_up, w_gate_up_scale, w_down, w_down_scale, w_dtype))
+    return EAAS_ERR_INVALID_ARG;
+  const WsLayout L = layout(*s);
+  if (!ws || !aligned16(ws) || ws_bytes < L.seg_total) return EAAS_ERR_WORKSPACE;
+  char* base = static_cast<char*>(ws);
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  const int cap = s->T;
+  uint16_t* x_cat = reinterpret_cast<uint16_t*>(base + L.x_cat);
+  int32_t* ids_cat = reinterpret_cast<int32_t*>(base + L.ids_cat);
+  float* w_cat = reinterpret_cast<float*>(base + L.w_cat);
+  hipError_t e = launch_seg_gather(segs, num_tokens, n_seg, cap, s->H, s->k, x_cat, ids_cat,
+                                   w_cat, hs);
+  if (e != hipSuccess) return EAAS_ERR_HIP;
+  const eaas_routing rt = ws_routing(base, L);
+  e = launch_route_permute(ids_cat, cap * s->k, s->E, rt,
+                           reinterpret_cast<int32_t*>(base + L.hist), hs);
+  if (e != hipSuccess) return EAAS_ERR_HIP;
+  float* stage = reinterpret_cast<float*>(base + L.stage);
+  FfnArgs a{};
+  a.T = cap; a.H = s->H; a.I = s->I; a.E = s->E; a.k = s->k;
+  a.x = x_cat;
+  a.perm = rt.perm;
+  a.offsets = rt.offsets;
+  a.active = rt.active;
+  a.w_gate_up = w_gate_up;
+  a.s_gate_up = w_gate_up_scale;
+  a.w_down = w_down;
+  a.s_down = w_down_scale;
+  a.fp8 = w_dtype == EAAS_FP8_E4M3;
+  a.h = reinterpret_cast<uint16_t*>(base + L.h);
+  a.y = stage;
+  a.topk_weights = w_cat;
+  a.epilogue = kDownWeighted;
+  e = launch_gate_up(a, hs);
+  if (e == hipSuccess) e = launch_down(a, hs);
+  if (e == hipSuccess)
+    e = launch_seg_combine(segs, num_tokens, n_seg, cap, s->H, s->k, stage, rt.inv,
+                           out_dtype == EAAS_FP32, hs);
+  return hip_status(e);
 }
 
 const char* eaas_status_string(int status) {

@@ -12,6 +12,9 @@ namespace eaas {
 // Slots handled by one workgroup of the histogram and scatter kernels.
 constexpr int kRouteChunk = 2048;
 
+// Requests in one dynamic batch (their token counts sit in shared memory).
+constexpr int kMaxSegments = 1024;
+
 inline int route_blocks(int R) { return (R + kRouteChunk - 1) / kRouteChunk; }
 
 // Enqueue the three routing kernels.  `hist` holds route_blocks(R) * E ints.
@@ -51,5 +54,15 @@ hipError_t launch_down(const FfnArgs& a, hipStream_t stream);
 hipError_t launch_combine(const float* y, const int32_t* inv, const float* w,
                           int T, int H, int k, bool rows_by_slot_weighted,
                           void* out, bool out_fp32, hipStream_t stream);
+
+// Dynamic batch (Algorithm 1 walks): gather the requests' tokens into the
+// contiguous batch of `cap` rows (slots of unused capacity get id -1), and
+// write each request's weighted sums from the by-slot fp32 staging rows.
+hipError_t launch_seg_gather(const eaas_segment* segs, const int32_t* num_tokens, int n_seg,
+                             int cap, int H, int k, uint16_t* x_cat, int32_t* ids_cat,
+                             float* w_cat, hipStream_t stream);
+hipError_t launch_seg_combine(const eaas_segment* segs, const int32_t* num_tokens, int n_seg,
+                              int cap, int H, int k, const float* stage, const int32_t* inv,
+                              bool out_fp32, hipStream_t stream);
 
 }  // namespace eaas

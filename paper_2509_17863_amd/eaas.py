@@ -16,14 +16,16 @@ __all__ = [
     "library_path", "eaas_workspace_bytes", "eaas_route_permute",
     "eaas_expert_ffn_grouped", "eaas_unpermute_combine", "eaas_expert_forward",
     "eaas_status_string", "eaas_expert_forward_profiled", "alloc_routing",
-    "alloc_workspace", "EXPORTED",
+    "alloc_workspace", "EXPORTED", "eaas_segments_workspace_bytes",
+    "alloc_segments_workspace", "segment_table", "eaas_expert_forward_segments",
 ]
 
 EAAS_OK = 0
 EAAS_BF16, EAAS_FP8_E4M3, EAAS_FP32 = 0, 1, 2
 EXPORTED = ("eaas_workspace_bytes", "eaas_route_permute", "eaas_expert_ffn_grouped",
             "eaas_unpermute_combine", "eaas_expert_forward", "eaas_expert_forward_profiled",
-            "eaas_status_string")
+            "eaas_status_string", "eaas_segments_workspace_bytes",
+            "eaas_expert_forward_segments")
 
 _LIB_PATH = Path(__file__).resolve().parent / "libeaas.so"
 _lib = None
@@ -72,6 +74,11 @@ def lib() -> ctypes.CDLL:
         L.eaas_expert_forward_profiled.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32,
                                                    rp, vp, sz, vp, vp]
         L.eaas_expert_forward_profiled.restype = i32
+        L.eaas_segments_workspace_bytes.argtypes = [sp, i32]
+        L.eaas_segments_workspace_bytes.restype = sz
+        L.eaas_expert_forward_segments.argtypes = [sp, vp, vp, i32, vp, vp, vp, vp, i32, i32, vp,
+                                                   sz, vp]
+        L.eaas_expert_forward_segments.restype = i32
         L.eaas_status_string.argtypes = [i32]
         L.eaas_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -207,3 +214,42 @@ def eaas_expert_forward_profiled(*args, events, **kwargs) -> None:
         if e is not None and not e.cuda_event:
             e.record()  # torch creates the underlying HIP event lazily
     eaas_expert_forward(*args, events=events, **kwargs)
+
+
+# ------------------------------------------------------------ dynamic batch
+def eaas_segments_workspace_bytes(T, H, I, E, k, w_dtype=EAAS_BF16) -> int:
+    s = _shape(T, H, I, E, k)
+    return int(lib().eaas_segments_workspace_bytes(ctypes.byref(s), int(w_dtype)))
+
+
+def alloc_segments_workspace(T, H, I, E, k, w_dtype=EAAS_BF16, device="cuda") -> torch.Tensor:
+    n = eaas_segments_workspace_bytes(T, H, I, E, k, w_dtype)
+    if n == 0:
+        raise EaasError(-2, "eaas_segments_workspace_bytes")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def segment_table(segments, device="cuda") -> torch.Tensor:
+    """Device array of eaas_segment records ([n, 4] int64: x, topk_ids,
+    topk_weights, out pointers) for a list of (x, topk_ids, topk_weights, out)
+    tensors.  Build it once per set of buffers; the token counts are passed
+    separately, so the same table serves every step."""
+    rows = [[_p(x), _p(ids), _p(w), _p(out)] for (x, ids, w, out) in segments]
+    t = torch.tensor(rows if rows else [[0, 0, 0, 0]], dtype=torch.int64)
+    return t.to(device)
+
+
+def eaas_expert_forward_segments(table: torch.Tensor, num_tokens: torch.Tensor, n_seg: int,
+                                 capacity: int, k: int, w_gate_up: torch.Tensor,
+                                 w_down: torch.Tensor, ws: torch.Tensor, out_dtype=EAAS_BF16,
+                                 w_gate_up_scale=None, w_down_scale=None, stream=None) -> None:
+    """The step on a dynamic batch: `table` from segment_table, `num_tokens`
+    a device int32 tensor of the requests' token counts (read on the device),
+    `capacity` the bound on their sum."""
+    E, twoI, H = w_gate_up.shape
+    s = _shape(capacity, H, twoI // 2, E, k)
+    st = lib().eaas_expert_forward_segments(
+        ctypes.byref(s), _p(table), _p(num_tokens), int(n_seg), _p(w_gate_up),
+        _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up), int(out_dtype),
+        _p(ws), ws.numel(), _stream(stream))
+    _check(st, "eaas_expert_forward_segments")

@@ -122,3 +122,42 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(eaas, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         eaas.lib()
+
+
+def test_segments_workspace_exceeds_single_batch():
+    T, H, I, E, k = 100, 512, 256, 8, 4
+    single = eaas.eaas_workspace_bytes(T, H, I, E, k)
+    seg = eaas.eaas_segments_workspace_bytes(T, H, I, E, k)
+    # the gathered batch (x rows, ids, scores) comes on top
+    assert seg >= single + T * H * 2 + 2 * T * k * 4
+    s = shape(H=200)
+    assert eaas.lib().eaas_segments_workspace_bytes(ctypes.byref(s), 0) == 0
+
+
+def test_forward_segments_rejects_bad_args():
+    L = eaas.lib()
+    s = shape()
+    ws = 1 << 30
+    args = lambda **kw: dict(dict(s=ctypes.byref(s), segs=FAKE, n=FAKE, n_seg=3, wgu=FAKE, sgu=None,  # noqa: E731
+                                  wd=FAKE, sd=None, wdt=0, odt=0, ws=FAKE, wsb=ws), **kw)
+
+    def call(a):
+        return L.eaas_expert_forward_segments(a["s"], a["segs"], a["n"], a["n_seg"], a["wgu"],
+                                              a["sgu"], a["wd"], a["sd"], a["wdt"], a["odt"],
+                                              a["ws"], a["wsb"], None)
+    assert call(args(s=None)) == -1
+    assert call(args(n_seg=-1)) == -1
+    assert call(args(n_seg=1025)) == -1
+    assert call(args(segs=None)) == -1
+    assert call(args(n=None)) == -1
+    assert call(args(odt=1)) == -1            # fp8 is not an output type
+    assert call(args(wdt=1)) == -1            # fp8 weights without scales
+    assert call(args(wgu=FAKE + 8)) == -1     # misaligned weights
+    assert call(args(ws=None)) == -3
+    assert call(args(wsb=64)) == -3
+    bad = shape(I=100)
+    assert call(args(s=ctypes.byref(bad))) == -2
+    # nothing to do: no requests, or no capacity
+    assert call(args(n_seg=0, segs=None, n=None)) == 0
+    empty = shape(T=0)
+    assert call(args(s=ctypes.byref(empty), segs=None, n=None)) == 0
