@@ -109,6 +109,43 @@ def cpu_baseline(d: dict, target_s: float = 12.0) -> dict:
                       f"sub-batch, fp64 BLAS, {t:.1f} s; weights converted to fp64 beforehand)"}
 
 
+def time_segments(d: dict, dev: dict, clients: int, steps: int, warmup: int, ms_single: float):
+    """The same batch as `clients` requests in separate buffers, through
+    eaas_expert_forward_segments (counts on the device, capacity T)."""
+    import torch
+
+    from paper_2509_17863_amd import eaas
+
+    T, H, I, E, k = d["T"], d["H"], d["I"], d["E"], d["k"]
+    bounds = np.linspace(0, T, clients + 1).astype(int)
+    bufs = []
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        bufs.append((dev["x"][a:b].clone(), dev["topk_ids"][a:b].clone(),
+                     dev["topk_weights"][a:b].clone(),
+                     torch.empty((max(b - a, 1), H), dtype=torch.bfloat16, device="cuda")))
+    table = eaas.segment_table(bufs)
+    counts = torch.tensor(np.diff(bounds), dtype=torch.int32, device="cuda")
+    wdt = eaas.EAAS_FP8_E4M3 if d["wdtype"] == "fp8" else eaas.EAAS_BF16
+    ws = eaas.alloc_segments_workspace(T, H, I, E, k, wdt)
+
+    def step():
+        eaas.eaas_expert_forward_segments(table, counts, clients, T, k, dev["w_gate_up"],
+                                          dev["w_down"], ws, eaas.EAAS_BF16,
+                                          dev["w_gate_up_scale"], dev["w_down_scale"])
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    return {"entry": "eaas_expert_forward_segments", "clients": clients,
+            "tokens_per_client": f"{int(np.diff(bounds).min())}-{int(np.diff(bounds).max())}",
+            "ms_per_step": round(ms, 4), "value": round(T / (ms * 1e-3), 1), "unit": "tokens/s",
+            "vs_single_batch": round(ms / ms_single, 4)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -116,6 +153,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mixtral")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--clients", type=int, default=0,
+                    help="also time the dynamic-batch entry point with the batch split into "
+                         "this many client requests (token counts read on the device)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one expert server on one GPU; --gpus {args.gpus} is not "
@@ -204,6 +244,8 @@ def main() -> int:
         "down_tflops": round(alg["dn_flops"] / (t_dn * 1e-3) / 1e12, 1),
         "roofline": roof,
     }
+    if args.clients > 0:
+        res["segments"] = time_segments(d, dev, args.clients, args.steps, args.warmup, ms)
     if hbm_bound:
         res["step_hbm_gbs"] = round((alg["gu_bytes"] + alg["dn_bytes"]) / (ms * 1e-3) / 1e9, 1)
     if not args.no_cpu_baseline:
