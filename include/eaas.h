@@ -219,6 +219,68 @@ int eaas_expert_forward_segments(const eaas_shape *s, const eaas_segment *segs,
                                  int w_dtype, int out_dtype, void *ws,
                                  size_t ws_bytes, void *stream);
 
+/*
+ * One server step over the clients' buffer slots (§3.2 "Shared Communication
+ * Buffer Design", §3.3 "Asynchronous Server Operation", §3.4 offline clients).
+ *
+ * Every client owns one slot on the server, in device memory:
+ *   flag      slot state, one of the eaas_slot_state values; the paper uses
+ *             one byte, here it is a 32-bit word so that host and device can
+ *             update it with naturally aligned atomic accesses
+ *   header    [2] int32: layer_id, batch_size
+ *   x         [capacity,H] bf16 hidden states; the step overwrites rows
+ *             [0, n) with the request's weighted sums (the results are written
+ *             back into the data payload, §3.3)
+ *   topk_ids, topk_weights  [capacity,k] int32 / fp32 (payload, §3.2)
+ * A server may hold several layers: layers[L] holds the weights of layer L
+ * (the arrays and dtype of eaas_expert_forward), and requests of different
+ * layers are batched into one grouped step (expert e of layer L is group
+ * L*E + e).
+ */
+enum eaas_slot_state {
+  EAAS_SLOT_EMPTY = 0,   /* the client may write a request                   */
+  EAAS_SLOT_READY = 1,   /* client write done: the server may take it         */
+  EAAS_SLOT_DONE = 2,    /* server computation done: the client may read      */
+  EAAS_SLOT_OFFLINE = 3  /* client reported offline: the server leaves it alone */
+};
+
+typedef struct eaas_slot {
+  int32_t *flag;
+  const int32_t *header;
+  void *x;
+  const int32_t *topk_ids;
+  const float *topk_weights;
+  int64_t capacity;
+} eaas_slot;
+
+typedef struct eaas_layer_weights {
+  const void *w_gate_up;
+  const float *w_gate_up_scale;
+  const void *w_down;
+  const float *w_down_scale;
+} eaas_layer_weights;
+
+/* Workspace bytes of eaas_server_step (0 for a shape the library rejects). */
+size_t eaas_server_workspace_bytes(const eaas_shape *s, int n_layers, int w_dtype);
+
+/* One server step: snapshot the slot flags, take the ready slots (flag 1) in
+ * slot order while their batch sizes (clamped to [0, capacity]) fit the step
+ * capacity s->T, run them as one dynamic batch, write each request's weighted
+ * sums (bf16) over its hidden states, then set the taken slots' flags to 2.
+ *   s->E        experts per layer; n_layers * s->E <= 1024
+ *   slots       [n_slots] eaas_slot, a DEVICE array; n_slots 0..1024
+ *   layers      [n_layers] eaas_layer_weights, a DEVICE array, all of w_dtype
+ * Slots in any other state, ready slots that do not fit (they stay ready for a
+ * later step), and payload rows past a request are not written.  A taken
+ * request whose layer_id names no layer of this server gets zeros.  Within a
+ * taken request, every row equals eaas_expert_forward on the requests of its
+ * layer concatenated in slot order.  The flags are written after all results,
+ * behind a system-scope fence.  Two steps over the same slots must not
+ * overlap in time (a later step runs on the same stream or after the first). */
+int eaas_server_step(const eaas_shape *s, const eaas_slot *slots, int n_slots,
+                     const eaas_layer_weights *layers, int n_layers, int w_dtype,
+                     void *ws, size_t ws_bytes, void *stream);
+
 /* Static, human-readable name of a status code. */
 const char *eaas_status_string(int status);
 

@@ -248,8 +248,8 @@ int eaas_expert_forward_segments(const eaas_shape* s, const eaas_segment* segs,
   uint16_t* x_cat = reinterpret_cast<uint16_t*>(base + L.x_cat);
   int32_t* ids_cat = reinterpret_cast<int32_t*>(base + L.ids_cat);
   float* w_cat = reinterpret_cast<float*>(base + L.w_cat);
-  hipError_t e = launch_seg_gather(segs, num_tokens, n_seg, cap, s->H, s->k, x_cat, ids_cat,
-                                   w_cat, hs);
+  hipError_t e = launch_seg_gather(segs, num_tokens, n_seg, cap, s->H, s->k, nullptr, s->E,
+                                   x_cat, ids_cat, w_cat, hs);
   if (e != hipSuccess) return EAAS_ERR_HIP;
   const eaas_routing rt = ws_routing(base, L);
   e = launch_route_permute(ids_cat, cap * s->k, s->E, rt,
@@ -277,6 +277,105 @@ int eaas_expert_forward_segments(const eaas_shape* s, const eaas_segment* segs,
     e = launch_seg_combine(segs, num_tokens, n_seg, cap, s->H, s->k, stage, rt.inv,
                            out_dtype == EAAS_FP32, hs);
   return hip_status(e);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Server-step extras after the dynamic-batch layout: the request records of
+// the taken slots, their counts, layer group offsets and the taken mask.
+struct SlotLayout {
+  size_t segs, counts, id_off, taken, total;
+};
+
+SlotLayout slot_layout(size_t seg_total) {
+  SlotLayout S{};
+  size_t o = seg_total;
+  S.segs = o;   o = align_up(o + (size_t)kMaxSegments * sizeof(eaas_segment));
+  S.counts = o; o = align_up(o + (size_t)kMaxSegments * 4);
+  S.id_off = o; o = align_up(o + (size_t)kMaxSegments * 4);
+  S.taken = o;  o = align_up(o + (size_t)kMaxSegments * 4);
+  S.total = o;
+  return S;
+}
+
+// The step's shape over all layers: one group per (layer, expert).
+int server_shape(const eaas_shape* s, int n_layers, eaas_shape* g) {
+  int st = check_shape(s);
+  if (st != EAAS_OK) return st;
+  if (n_layers < 1) return EAAS_ERR_INVALID_ARG;
+  if ((long long)n_layers * s->E > kMaxExperts) return EAAS_ERR_UNSUPPORTED;
+  *g = *s;
+  g->E = n_layers * s->E;
+  return check_shape(g);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t eaas_server_workspace_bytes(const eaas_shape* s, int n_layers, int w_dtype) {
+  eaas_shape g;
+  if (server_shape(s, n_layers, &g) != EAAS_OK) return 0;
+  if (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3) return 0;
+  return slot_layout(layout(g).seg_total).total;
+}
+
+int eaas_server_step(const eaas_shape* s, const eaas_slot* slots, int n_slots,
+                     const eaas_layer_weights* layers, int n_layers, int w_dtype, void* ws,
+                     size_t ws_bytes, void* stream) {
+  eaas_shape g;
+  int st = server_shape(s, n_layers, &g);
+  if (st != EAAS_OK) return st;
+  if (n_slots < 0 || n_slots > kMaxSegments) return EAAS_ERR_INVALID_ARG;
+  if (n_slots == 0) return EAAS_OK;
+  if (!slots || !layers || (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3))
+    return EAAS_ERR_INVALID_ARG;
+  const WsLayout L = layout(g);
+  const SlotLayout SL = slot_layout(L.seg_total);
+  if (!ws || !aligned16(ws) || ws_bytes < SL.total) return EAAS_ERR_WORKSPACE;
+  char* base = static_cast<char*>(ws);
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  const int cap = s->T;
+  eaas_segment* segs = reinterpret_cast<eaas_segment*>(base + SL.segs);
+  int32_t* counts = reinterpret_cast<int32_t*>(base + SL.counts);
+  int32_t* id_off = reinterpret_cast<int32_t*>(base + SL.id_off);
+  int32_t* taken = reinterpret_cast<int32_t*>(base + SL.taken);
+  hipError_t e = launch_slot_snapshot(slots, n_slots, cap, n_layers, s->E, segs, counts, id_off,
+                                      taken, hs);
+  if (e != hipSuccess) return EAAS_ERR_HIP;
+  if (cap > 0) {
+    uint16_t* x_cat = reinterpret_cast<uint16_t*>(base + L.x_cat);
+    int32_t* ids_cat = reinterpret_cast<int32_t*>(base + L.ids_cat);
+    float* w_cat = reinterpret_cast<float*>(base + L.w_cat);
+    e = launch_seg_gather(segs, counts, n_slots, cap, g.H, g.k, id_off, s->E, x_cat, ids_cat,
+                          w_cat, hs);
+    if (e != hipSuccess) return EAAS_ERR_HIP;
+    const eaas_routing rt = ws_routing(base, L);
+    e = launch_route_permute(ids_cat, cap * g.k, g.E, rt,
+                             reinterpret_cast<int32_t*>(base + L.hist), hs);
+    if (e != hipSuccess) return EAAS_ERR_HIP;
+    FfnArgs a{};
+    a.T = cap; a.H = g.H; a.I = g.I; a.E = g.E; a.k = g.k;
+    a.x = x_cat;
+    a.perm = rt.perm;
+    a.offsets = rt.offsets;
+    a.active = rt.active;
+    a.fp8 = w_dtype == EAAS_FP8_E4M3;
+    a.h = reinterpret_cast<uint16_t*>(base + L.h);
+    a.y = reinterpret_cast<float*>(base + L.stage);
+    a.topk_weights = w_cat;
+    a.epilogue = kDownWeighted;
+    a.layers = layers;
+    a.e_layer = s->E;
+    e = launch_gate_up(a, hs);
+    if (e == hipSuccess) e = launch_down(a, hs);
+    if (e == hipSuccess)
+      e = launch_seg_combine(segs, counts, n_slots, cap, g.H, g.k, a.y, rt.inv, false, hs);
+    if (e != hipSuccess) return EAAS_ERR_HIP;
+  }
+  return hip_status(launch_slot_complete(slots, n_slots, taken, hs));
 }
 
 const char* eaas_status_string(int status) {

@@ -70,8 +70,31 @@ struct GemmParams {
   float* y;               // down output [R, N]
   const float* w;         // [R] router scores by slot
   int R;                  // slots (T*k)
-  int E;                  // resident experts
+  int E;                  // resident experts (groups)
+  // server step over several layers: group e is expert e % e_layer of layer
+  // e / e_layer, whose weights come from that layer's record instead of b
+  const eaas_layer_weights* layers;  // nullptr: one weight array (b, b_scale)
+  int e_layer;
+  bool down;              // the records' down-projection members
 };
+
+// Weights of group e ([N, K], bf16 or fp8 bytes of esz each).
+__device__ __forceinline__ const uint8_t* group_weights(const GemmParams& p, int e, int esz) {
+  if (p.layers == nullptr) return p.b + (size_t)e * p.N * p.K * esz;
+  const int L = e / p.e_layer;
+  const eaas_layer_weights& lw = p.layers[L];
+  return static_cast<const uint8_t*>(p.down ? lw.w_down : lw.w_gate_up) +
+         (size_t)(e - L * p.e_layer) * p.N * p.K * esz;
+}
+
+// fp8 block scales of group e ([N/128, K/128]).
+__device__ __forceinline__ const float* group_scales(const GemmParams& p, int e) {
+  const size_t per = (size_t)(p.N / 128) * (p.K / 128);
+  if (p.layers == nullptr) return p.b_scale + (size_t)e * per;
+  const int L = e / p.e_layer;
+  const eaas_layer_weights& lw = p.layers[L];
+  return (p.down ? lw.w_down_scale : lw.w_gate_up_scale) + (size_t)(e - L * p.e_layer) * per;
+}
 
 struct Tile {
   int e;           // expert
@@ -608,7 +631,7 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   typename Full::Src src;
   src.wave = wave;
   src.a = reinterpret_cast<const char*>(p.a);
-  src.b = reinterpret_cast<const char*>(p.b) + (size_t)t.e * p.N * p.K * (FP8 ? 1 : 2);
+  src.b = reinterpret_cast<const char*>(group_weights(p, t.e, FP8 ? 1 : 2));
   {
     const int drow = lane / CH;
     const int dpc = lane % CH;
@@ -644,8 +667,8 @@ void grouped_gemm_dma_kernel(GemmParams p) {
     const int br = block_row<GATEUP, BN, NBW>(wn, j);
     b_lane_off[j] = (br + lrow) * BRB;
     sc[j] = FP8 ? (const CONST_AS float*)wave_uniform(
-                      p.b_scale + ((size_t)t.e * (p.N / 128) +
-                                   weight_row<GATEUP, BN>(p, t.tn, br) / 128) * (p.K / 128))
+                      group_scales(p, t.e) +
+                      (size_t)(weight_row<GATEUP, BN>(p, t.tn, br) / 128) * (p.K / 128))
                 : nullptr;
   }
   const int s_l = swz<RB>(lrow);
@@ -728,7 +751,7 @@ void grouped_gemm_kernel(GemmParams p) {
     a_off[i] = src_row * p.lda + a_chunk * 8;
   }
   const size_t esz = FP8 ? 1 : 2;
-  const uint8_t* bexp = p.b + (size_t)e * p.N * p.K * esz;
+  const uint8_t* bexp = group_weights(p, e, (int)esz);
   constexpr int B_CHUNKS = FP8 ? 4 : 8;  // 16-byte chunks per 64-wide K slice
   const int b_chunk = tid % B_CHUNKS;
   int b_off[B_LOADS];
@@ -830,7 +853,7 @@ void grouped_gemm_kernel(GemmParams p) {
     if (FP8 && (kt & 1)) {
       // end of a 128-wide K block: acc += scale * partial
       const int kb = kt >> 1;
-      const float* sexp = p.b_scale + (size_t)e * (p.N / 128) * (p.K / 128);
+      const float* sexp = group_scales(p, e);
 #pragma unroll
       for (int j = 0; j < NBW; ++j) {
         const int wrow = weight_row<GATEUP, BN>(p, tn, bn0[j]);
@@ -951,7 +974,7 @@ void grouped_gemm_pp_kernel(GemmParams p) {
         doff[q] = (uint32_t)(src_row * p.lda + ((dpc ^ swz<RB>(row)) * 8)) * 2u;
       }
     } else {
-      dbase = reinterpret_cast<const char*>(p.b) + (size_t)t.e * p.N * p.K * 2;
+      dbase = reinterpret_cast<const char*>(group_weights(p, t.e, 2));
 #pragma unroll
       for (int q = 0; q < INST; ++q) {
         const int j = (w4 + 4 * q) * 8 + drow;
@@ -1122,6 +1145,8 @@ GemmParams common_params(const FfnArgs& a) {
   g.w = a.topk_weights;
   g.R = a.T * a.k;
   g.E = a.E;
+  g.layers = a.layers;
+  g.e_layer = a.e_layer;
   return g;
 }
 
@@ -1157,6 +1182,7 @@ hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
   g.N = a.H;
   g.K = a.I;
   g.y = a.y;
+  g.down = true;
   const int R = a.T * a.k;
   const bool sm = small_rows(a);
   if (a.epilogue == kDownWeighted)

@@ -43,6 +43,10 @@ struct FfnArgs {
   float* y;                   // [R,H] fp32
   const float* topk_weights;  // [R] (weighted epilogue)
   int epilogue;               // DownEpilogue
+  // server step over several layers: E = layers x e_layer groups whose weights
+  // come from the per-layer records (w_* and s_* above are then unused)
+  const eaas_layer_weights* layers = nullptr;
+  int e_layer = 0;
 };
 
 // Gate/up GEMM with the SiLU*mul epilogue into h.
@@ -58,11 +62,22 @@ hipError_t launch_combine(const float* y, const int32_t* inv, const float* w,
 // Dynamic batch (Algorithm 1 walks): gather the requests' tokens into the
 // contiguous batch of `cap` rows (slots of unused capacity get id -1), and
 // write each request's weighted sums from the by-slot fp32 staging rows.
+// id_off (optional): per request, the group offset of its ids (valid ids are
+// those in [0, e_local)); a negative offset masks the request's slots.
 hipError_t launch_seg_gather(const eaas_segment* segs, const int32_t* num_tokens, int n_seg,
-                             int cap, int H, int k, uint16_t* x_cat, int32_t* ids_cat,
-                             float* w_cat, hipStream_t stream);
+                             int cap, int H, int k, const int32_t* id_off, int e_local,
+                             uint16_t* x_cat, int32_t* ids_cat, float* w_cat,
+                             hipStream_t stream);
 hipError_t launch_seg_combine(const eaas_segment* segs, const int32_t* num_tokens, int n_seg,
                               int cap, int H, int k, const float* stage, const int32_t* inv,
                               bool out_fp32, hipStream_t stream);
+
+// Server step: snapshot the slots into a dynamic batch (records, counts,
+// layer group offsets, taken mask), and mark the taken slots done.
+hipError_t launch_slot_snapshot(const eaas_slot* slots, int n_slots, int cap, int n_layers,
+                                int e_layer, eaas_segment* segs, int32_t* num_tokens,
+                                int32_t* id_off, int32_t* taken, hipStream_t stream);
+hipError_t launch_slot_complete(const eaas_slot* slots, int n_slots, const int32_t* taken,
+                                hipStream_t stream);
 
 }  // namespace eaas

@@ -36,10 +36,12 @@ __device__ __forceinline__ void load_counts(const int32_t* num_tokens, int n_seg
   __syncthreads();
 }
 
+// id_off (optional, per request): valid ids e in [0, e_local) become group
+// id_off[b] + e; a negative id_off masks every slot of the request.
 __global__ __launch_bounds__(kSegThreads) void seg_gather_kernel(
     const eaas_segment* __restrict__ segs, const int32_t* __restrict__ num_tokens, int n_seg,
-    int cap, int H, int k, uint16_t* __restrict__ x_cat, int32_t* __restrict__ ids_cat,
-    float* __restrict__ w_cat) {
+    int cap, int H, int k, const int32_t* __restrict__ id_off, int e_local,
+    uint16_t* __restrict__ x_cat, int32_t* __restrict__ ids_cat, float* __restrict__ w_cat) {
   __shared__ int s_n[kMaxSegments];
   load_counts(num_tokens, n_seg, s_n);
   const int row_chunks = H / 8;  // 16-byte chunks of a bf16 row
@@ -49,6 +51,7 @@ __global__ __launch_bounds__(kSegThreads) void seg_gather_kernel(
     const int n = clamp_count(s_n[b], base, cap);
     if (token_id < n) {
       const eaas_segment sg = segs[b];
+      const int off = id_off ? id_off[b] : 0;
       const u32x4* src = static_cast<const u32x4*>(sg.x);
       while (token_id < n) {
         const size_t g = (size_t)base + token_id;
@@ -56,7 +59,9 @@ __global__ __launch_bounds__(kSegThreads) void seg_gather_kernel(
         u32x4* drow = reinterpret_cast<u32x4*>(x_cat + g * H);
         for (int c = threadIdx.x; c < row_chunks; c += blockDim.x) drow[c] = srow[c];
         for (int j = threadIdx.x; j < k; j += blockDim.x) {
-          ids_cat[g * k + j] = sg.topk_ids[(size_t)token_id * k + j];
+          int id = sg.topk_ids[(size_t)token_id * k + j];
+          if (id_off) id = (off >= 0 && (unsigned)id < (unsigned)e_local) ? off + id : -1;
+          ids_cat[g * k + j] = id;
           w_cat[g * k + j] = sg.topk_weights[(size_t)token_id * k + j];
         }
         token_id += gridDim.x;
@@ -115,16 +120,95 @@ __global__ __launch_bounds__(kSegThreads) void seg_combine_kernel(
   }
 }
 
+// Server step, first kernel (one workgroup, thread b = slot b): snapshot the
+// flags with system-scope acquire loads, take the ready slots in slot order
+// while the running token total fits the capacity (an inclusive scan of the
+// ready slots' clamped batch sizes: once it passes the capacity it stays
+// past it, so every later ready slot waits for a later step), and lay out the
+// taken requests as a dynamic batch: request records, token counts, and the
+// group offset of the request's layer.
+__global__ __launch_bounds__(kMaxSegments) void slot_snapshot_kernel(
+    const eaas_slot* __restrict__ slots, int n_slots, int cap, int n_layers, int e_layer,
+    eaas_segment* __restrict__ segs, int32_t* __restrict__ num_tokens,
+    int32_t* __restrict__ id_off, int32_t* __restrict__ taken) {
+  __shared__ long long s_wave[kMaxSegments / kWave];
+  const int b = threadIdx.x;
+  const int lane = b & (kWave - 1), wave = b / kWave;
+  bool ready = false;
+  long long cnt = 0;  // counts are summed in 64 bits: 1024 of them can pass 2^31
+  int layer = -1;
+  eaas_slot sl{};
+  if (b < n_slots) {
+    sl = slots[b];
+    const int f = __hip_atomic_load(sl.flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (f == EAAS_SLOT_READY) {
+      ready = true;
+      layer = sl.header[0];
+      cnt = max(0LL, min((long long)sl.header[1], (long long)sl.capacity));
+    }
+  }
+  long long incl = cnt;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const long long o = __shfl_up(incl, d, kWave);
+    if (lane >= d) incl += o;
+  }
+  if (lane == kWave - 1) s_wave[wave] = incl;
+  __syncthreads();
+  long long run = incl;
+  for (int w = 0; w < wave; ++w) run += s_wave[w];
+  if (b < n_slots) {
+    const bool take = ready && run <= cap;
+    taken[b] = take;
+    num_tokens[b] = take ? (int)cnt : 0;
+    id_off[b] = (layer >= 0 && layer < n_layers) ? layer * e_layer : -1;
+    eaas_segment sg;
+    sg.x = sl.x;
+    sg.topk_ids = sl.topk_ids;
+    sg.topk_weights = sl.topk_weights;
+    sg.out = sl.x;
+    segs[b] = sg;
+  }
+}
+
+// Server step, last kernel: the taken slots' flags become "server
+// computation done", after a system-scope fence over the results (this
+// kernel runs after the combine on the same stream).
+__global__ __launch_bounds__(kMaxSegments) void slot_complete_kernel(
+    const eaas_slot* __restrict__ slots, int n_slots, const int32_t* __restrict__ taken) {
+  const int b = threadIdx.x;
+  if (b >= n_slots || !taken[b]) return;
+  __threadfence_system();
+  __hip_atomic_store(slots[b].flag, (int)EAAS_SLOT_DONE, __ATOMIC_RELEASE,
+                     __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 // Static grids: sized from the capacity alone (Algorithm 1 needs no counts).
 inline unsigned seg_grid(int cap) { return (unsigned)max(1, min(cap, 2048)); }
 
 }  // namespace
 
 hipError_t launch_seg_gather(const eaas_segment* segs, const int32_t* num_tokens, int n_seg,
-                             int cap, int H, int k, uint16_t* x_cat, int32_t* ids_cat,
-                             float* w_cat, hipStream_t stream) {
+                             int cap, int H, int k, const int32_t* id_off, int e_local,
+                             uint16_t* x_cat, int32_t* ids_cat, float* w_cat,
+                             hipStream_t stream) {
   hipLaunchKernelGGL(seg_gather_kernel, dim3(seg_grid(cap)), dim3(kSegThreads), 0, stream, segs,
-                     num_tokens, n_seg, cap, H, k, x_cat, ids_cat, w_cat);
+                     num_tokens, n_seg, cap, H, k, id_off, e_local, x_cat, ids_cat, w_cat);
+  return hipGetLastError();
+}
+
+hipError_t launch_slot_snapshot(const eaas_slot* slots, int n_slots, int cap, int n_layers,
+                                int e_layer, eaas_segment* segs, int32_t* num_tokens,
+                                int32_t* id_off, int32_t* taken, hipStream_t stream) {
+  hipLaunchKernelGGL(slot_snapshot_kernel, dim3(1), dim3(kMaxSegments), 0, stream, slots,
+                     n_slots, cap, n_layers, e_layer, segs, num_tokens, id_off, taken);
+  return hipGetLastError();
+}
+
+hipError_t launch_slot_complete(const eaas_slot* slots, int n_slots, const int32_t* taken,
+                                hipStream_t stream) {
+  hipLaunchKernelGGL(slot_complete_kernel, dim3(1), dim3(kMaxSegments), 0, stream, slots,
+                     n_slots, taken);
   return hipGetLastError();
 }
 

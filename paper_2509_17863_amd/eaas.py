@@ -18,14 +18,18 @@ __all__ = [
     "eaas_status_string", "eaas_expert_forward_profiled", "alloc_routing",
     "alloc_workspace", "EXPORTED", "eaas_segments_workspace_bytes",
     "alloc_segments_workspace", "segment_table", "eaas_expert_forward_segments",
+    "EAAS_SLOT_EMPTY", "EAAS_SLOT_READY", "EAAS_SLOT_DONE", "EAAS_SLOT_OFFLINE",
+    "eaas_server_workspace_bytes", "alloc_server_workspace", "slot_table", "layer_table",
+    "eaas_server_step",
 ]
 
 EAAS_OK = 0
 EAAS_BF16, EAAS_FP8_E4M3, EAAS_FP32 = 0, 1, 2
+EAAS_SLOT_EMPTY, EAAS_SLOT_READY, EAAS_SLOT_DONE, EAAS_SLOT_OFFLINE = 0, 1, 2, 3
 EXPORTED = ("eaas_workspace_bytes", "eaas_route_permute", "eaas_expert_ffn_grouped",
             "eaas_unpermute_combine", "eaas_expert_forward", "eaas_expert_forward_profiled",
             "eaas_status_string", "eaas_segments_workspace_bytes",
-            "eaas_expert_forward_segments")
+            "eaas_expert_forward_segments", "eaas_server_workspace_bytes", "eaas_server_step")
 
 _LIB_PATH = Path(__file__).resolve().parent / "libeaas.so"
 _lib = None
@@ -79,6 +83,10 @@ def lib() -> ctypes.CDLL:
         L.eaas_expert_forward_segments.argtypes = [sp, vp, vp, i32, vp, vp, vp, vp, i32, i32, vp,
                                                    sz, vp]
         L.eaas_expert_forward_segments.restype = i32
+        L.eaas_server_workspace_bytes.argtypes = [sp, i32, i32]
+        L.eaas_server_workspace_bytes.restype = sz
+        L.eaas_server_step.argtypes = [sp, vp, i32, vp, i32, i32, vp, sz, vp]
+        L.eaas_server_step.restype = i32
         L.eaas_status_string.argtypes = [i32]
         L.eaas_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -253,3 +261,45 @@ def eaas_expert_forward_segments(table: torch.Tensor, num_tokens: torch.Tensor, 
         _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up), int(out_dtype),
         _p(ws), ws.numel(), _stream(stream))
     _check(st, "eaas_expert_forward_segments")
+
+
+# ------------------------------------------------------------ server step
+def eaas_server_workspace_bytes(T, H, I, E, k, n_layers, w_dtype=EAAS_BF16) -> int:
+    s = _shape(T, H, I, E, k)
+    return int(lib().eaas_server_workspace_bytes(ctypes.byref(s), int(n_layers), int(w_dtype)))
+
+
+def alloc_server_workspace(T, H, I, E, k, n_layers, w_dtype=EAAS_BF16,
+                           device="cuda") -> torch.Tensor:
+    n = eaas_server_workspace_bytes(T, H, I, E, k, n_layers, w_dtype)
+    if n == 0:
+        raise EaasError(-2, "eaas_server_workspace_bytes")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def slot_table(slots, device="cuda") -> torch.Tensor:
+    """Device array of eaas_slot records ([n, 6] int64) for a list of
+    (flag, header, x, topk_ids, topk_weights) device tensors; the capacity is
+    x's row count."""
+    rows = [[_p(f), _p(h), _p(x), _p(i), _p(w), int(x.shape[0])] for (f, h, x, i, w) in slots]
+    t = torch.tensor(rows if rows else [[0] * 6], dtype=torch.int64)
+    return t.to(device)
+
+
+def layer_table(layers, device="cuda") -> torch.Tensor:
+    """Device array of eaas_layer_weights records ([n, 4] int64) for a list of
+    (w_gate_up, w_gate_up_scale, w_down, w_down_scale) tensors (scales None
+    for bf16 weights)."""
+    rows = [[_p(a) or 0, _p(b) or 0, _p(c) or 0, _p(d) or 0] for (a, b, c, d) in layers]
+    return torch.tensor(rows, dtype=torch.int64).to(device)
+
+
+def eaas_server_step(slots: torch.Tensor, n_slots: int, layers: torch.Tensor, n_layers: int,
+                     capacity: int, H: int, I: int, E: int, k: int, ws: torch.Tensor,
+                     w_dtype=EAAS_BF16, stream=None) -> None:
+    """One server step over the slots of `slot_table` with the weights of
+    `layer_table` (E experts per layer)."""
+    s = _shape(capacity, H, I, E, k)
+    st = lib().eaas_server_step(ctypes.byref(s), _p(slots), int(n_slots), _p(layers),
+                                int(n_layers), int(w_dtype), _p(ws), ws.numel(), _stream(stream))
+    _check(st, "eaas_server_step")

@@ -161,3 +161,27 @@ def test_forward_segments_rejects_bad_args():
     assert call(args(n_seg=0, segs=None, n=None)) == 0
     empty = shape(T=0)
     assert call(args(s=ctypes.byref(empty), segs=None, n=None)) == 0
+
+
+def test_server_workspace_and_validation():
+    L = eaas.lib()
+    s = shape(E=32)
+    assert L.eaas_server_workspace_bytes(ctypes.byref(s), 32, 0) > 0
+    assert L.eaas_server_workspace_bytes(ctypes.byref(s), 33, 0) == 0   # 33*32 groups > 1024
+    assert L.eaas_server_workspace_bytes(ctypes.byref(s), 0, 0) == 0
+    assert L.eaas_server_workspace_bytes(ctypes.byref(s), 2, 2) == 0    # fp32 weights
+    ws = 1 << 30
+
+    def call(s_=ctypes.byref(s), slots=FAKE, n=4, layers=FAKE, nl=2, wdt=0, w=FAKE, wb=ws):
+        return L.eaas_server_step(s_, slots, n, layers, nl, wdt, w, wb, None)
+    assert call(s_=None) == -1
+    assert call(n=-1) == -1
+    assert call(n=1025) == -1
+    assert call(slots=None) == -1
+    assert call(layers=None) == -1
+    assert call(nl=0) == -1
+    assert call(nl=40) == -2
+    assert call(wdt=2) == -1
+    assert call(w=None) == -3
+    assert call(wb=128) == -3
+    assert call(n=0, slots=None, layers=None) == 0

@@ -1,0 +1,214 @@
+"""GPU parity of the server step over client buffer slots (EaaS §3.2 flags and
+header, §3.3 server loop, §3.4 offline clients), through the C ABI.
+
+The flags after a step, and every byte of the slots the step must not write,
+are compared with the slot-protocol oracle bit for bit.  The taken requests'
+rows must equal, bit for bit, eaas_expert_forward on the requests of the same
+layer concatenated in slot order (bf16 output), and stay within 2e-2 * RMS
+of the oracle.  Every case prints its name before touching the GPU.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import server_oracle as SV
+from paper_2509_17863_amd import eaas, synth
+from paper_2509_17863_amd.device_io import bf16_tensor_to_bits, to_device
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+H, I, E, K = 512, 256, 8, 4
+
+
+def say(*a):
+    print("[gpu-case]", *a, flush=True)
+
+
+def make_layers(n, wdtype="bf16", seed=60):
+    out = []
+    for L in range(n):
+        d = synth.make_inputs(1, H, I, E, K, seed + L, wdtype=wdtype)
+        out.append({key: d[key] for key in ("wdtype", "w_gate_up", "w_down", "w_gate_up_scale",
+                                            "w_down_scale")})
+    return out
+
+
+def make_slots(specs, seed=70):
+    """specs: (flag, layer, batch_size, capacity).  Payload rows are random;
+    ids include ids of other servers (out of range)."""
+    rng = np.random.default_rng(seed)
+    slots = []
+    for flag, layer, n, cap in specs:
+        x = synth.bf16_bits_from_f32(rng.standard_normal((cap, H)).astype(np.float32))
+        logits = rng.standard_normal((cap, E + 2))
+        ids = np.argsort(-logits, axis=1)[:, :K].astype(np.int32) - 1   # ids in [-1, E]
+        w = rng.random((cap, K)).astype(np.float32)
+        w /= w.sum(1, keepdims=True)
+        slots.append(dict(flag=flag, layer=layer, n=n, x=x, topk_ids=ids, topk_weights=w))
+    return slots
+
+
+class Server:
+    """Device-resident slots and layer weights, as a server would hold them."""
+
+    def __init__(self, slots, layers, capacity):
+        self.slots, self.layers, self.cap = slots, layers, capacity
+        self.wdt = eaas.EAAS_FP8_E4M3 if layers[0]["wdtype"] == "fp8" else eaas.EAAS_BF16
+        self.dl = [to_device(dict(lw, x=np.zeros((1, H), np.uint16),
+                                  topk_ids=np.zeros((1, K), np.int32),
+                                  topk_weights=np.zeros((1, K), np.float32))) for lw in layers]
+        self.ltab = eaas.layer_table([(d["w_gate_up"], d["w_gate_up_scale"], d["w_down"],
+                                       d["w_down_scale"]) for d in self.dl])
+        self.dev = []
+        for s in slots:
+            flag = torch.tensor([s["flag"]], dtype=torch.int32, device="cuda")
+            hdr = torch.tensor([s["layer"], s["n"]], dtype=torch.int32, device="cuda")
+            x = torch.from_numpy(s["x"].view(np.int16)).view(torch.bfloat16).cuda()
+            ids = torch.from_numpy(s["topk_ids"]).cuda()
+            w = torch.from_numpy(s["topk_weights"]).cuda()
+            self.dev.append((flag, hdr, x, ids, w))
+        self.stab = eaas.slot_table(self.dev)
+        self.ws = eaas.alloc_server_workspace(capacity, H, I, E, K, len(layers), self.wdt)
+
+    def step(self, stream=None):
+        eaas.eaas_server_step(self.stab, len(self.dev), self.ltab, len(self.layers), self.cap,
+                              H, I, E, K, self.ws, self.wdt, stream)
+
+    def state(self):
+        torch.cuda.synchronize()
+        return ([int(d[0].item()) for d in self.dev], [bf16_tensor_to_bits(d[2]) for d in self.dev])
+
+    def post(self, b, flag, layer, n):
+        """A client writes a new request header and sets its flag."""
+        self.slots[b].update(flag=flag, layer=layer, n=n)
+        self.dev[b][1].copy_(torch.tensor([layer, n], dtype=torch.int32))
+        self.dev[b][0].fill_(flag)
+
+
+def forward_layer_concat(slots, members, counts, lw):
+    """eaas_expert_forward (bf16 out) on the given requests concatenated."""
+    T = int(sum(counts[b] for b in members))
+    d = dict(lw, T=T, H=H, I=I, E=E, k=K,
+             x=np.concatenate([slots[b]["x"][: counts[b]] for b in members]),
+             topk_ids=np.concatenate([slots[b]["topk_ids"][: counts[b]] for b in members]),
+             topk_weights=np.concatenate([slots[b]["topk_weights"][: counts[b]] for b in members]))
+    dev = to_device(d)
+    wdt = eaas.EAAS_FP8_E4M3 if lw["wdtype"] == "fp8" else eaas.EAAS_BF16
+    ws = eaas.alloc_workspace(T, H, I, E, K, wdt)
+    out = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
+    eaas.eaas_expert_forward(dev["x"], dev["topk_ids"], dev["topk_weights"], dev["w_gate_up"],
+                             dev["w_down"], out, ws, dev["w_gate_up_scale"], dev["w_down_scale"])
+    torch.cuda.synchronize()
+    return bf16_tensor_to_bits(out)
+
+
+def check_step(srv, before):
+    """Compare the server's state after a step with the oracle's step from
+    the state `before` (list of slot dicts as they were)."""
+    want_flags, want_x, want_res = SV.server_step(before, srv.layers, E, srv.cap)
+    flags, xs = srv.state()
+    assert flags == want_flags.tolist()
+    taken, counts = SV.take_slots([s["flag"] for s in before], [s["n"] for s in before],
+                                  [s["x"].shape[0] for s in before], srv.cap)
+    for b, s in enumerate(before):
+        n = int(counts[b])
+        assert np.array_equal(xs[b][n:], s["x"][n:]), f"slot {b}: rows past the request"
+        if not taken[b]:
+            assert np.array_equal(xs[b], s["x"]), f"slot {b} was not taken but written"
+    for L, lw in enumerate(srv.layers):
+        members = [b for b in range(len(before)) if taken[b] and before[b]["layer"] == L and counts[b]]
+        if not members:
+            continue
+        ref = forward_layer_concat(before, members, counts, lw)
+        p = 0
+        for b in members:
+            n = int(counts[b])
+            assert np.array_equal(xs[b][:n], ref[p:p + n]), f"slot {b} vs concatenated forward"
+            got = (xs[b][:n].astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+            rms = float(np.sqrt((want_res[b] ** 2).mean()))
+            # bf16 output: one rounding of the result on top of the fp32 budget
+            assert np.abs(got - want_res[b]).max() <= TOL * rms + np.abs(want_res[b]).max() * 2 ** -8
+            p += n
+    for b, s in enumerate(before):
+        if taken[b] and counts[b] and not (0 <= s["layer"] < len(srv.layers)):
+            assert np.all(xs[b][: counts[b]] == 0)
+    # the host-side copy now mirrors the device
+    for b, s in enumerate(srv.slots):
+        s["flag"] = flags[b]
+        s["x"] = xs[b].copy()
+
+
+def snapshot(slots):
+    return [dict(s, x=s["x"].copy()) for s in slots]
+
+
+SPECS = [(1, 0, 40, 48), (0, 1, 30, 32), (1, 1, 64, 64), (3, 0, 20, 24), (1, 0, 0, 16),
+         (2, 1, 10, 16), (1, 7, 12, 16), (1, 1, 100, 128), (1, 0, 5, 8)]
+
+
+def test_server_step_mixed_states_and_layers(gpu):
+    layers = make_layers(2)
+    slots = make_slots(SPECS)
+    srv = Server(slots, layers, capacity=160)
+    say("server step bf16, 2 layers, 9 slots")
+    before = snapshot(srv.slots)
+    srv.step()
+    check_step(srv, before)
+    # slot 7 (100 tokens) did not fit: it is still ready and the next step takes it
+    assert srv.slots[7]["flag"] == eaas.EAAS_SLOT_READY
+    say("server second step")
+    before = snapshot(srv.slots)
+    srv.step()
+    check_step(srv, before)
+    assert srv.slots[7]["flag"] == eaas.EAAS_SLOT_DONE
+
+
+def test_server_step_fp8_three_layers(gpu):
+    layers = make_layers(3, wdtype="fp8", seed=61)
+    specs = [(1, L % 3, n, n + 4) for L, n in enumerate([17, 9, 33, 1, 64, 0, 12, 50])]
+    slots = make_slots(specs, seed=71)
+    srv = Server(slots, layers, capacity=256)
+    say("server step fp8, 3 layers")
+    before = snapshot(srv.slots)
+    srv.step()
+    check_step(srv, before)
+
+
+def test_server_step_nothing_ready(gpu):
+    layers = make_layers(1)
+    slots = make_slots([(0, 0, 5, 8), (3, 0, 5, 8), (2, 0, 5, 8)])
+    srv = Server(slots, layers, capacity=32)
+    say("server step nothing ready")
+    before = snapshot(srv.slots)
+    srv.step()
+    check_step(srv, before)
+
+
+def test_server_graph_replay_serves_new_requests(gpu):
+    layers = make_layers(2, seed=62)
+    slots = make_slots([(1, 0, 20, 32), (1, 1, 25, 32), (0, 0, 0, 32), (1, 0, 7, 32)], seed=72)
+    srv = Server(slots, layers, capacity=64)
+    say("server graph replay")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    before = snapshot(srv.slots)
+    with torch.cuda.stream(s):
+        srv.step(s)
+    torch.cuda.current_stream().wait_stream(s)
+    check_step(srv, before)
+    g = torch.cuda.CUDAGraph()
+    # capture a step while no slot is ready (capture does not run it)
+    with torch.cuda.graph(g):
+        srv.step()
+    rng = np.random.default_rng(5)
+    for rnd in range(4):
+        # clients read their results (flag 2 -> 0) and post new requests
+        for b in range(len(srv.slots)):
+            if srv.slots[b]["flag"] == eaas.EAAS_SLOT_DONE or rnd == 2:
+                n = int(rng.integers(0, 33))
+                srv.post(b, eaas.EAAS_SLOT_READY, int(rng.integers(0, 2)), n)
+        torch.cuda.synchronize()
+        before = snapshot(srv.slots)
+        g.replay()
+        check_step(srv, before)
