@@ -146,6 +146,50 @@ def time_segments(d: dict, dev: dict, clients: int, steps: int, warmup: int, ms_
             "vs_single_batch": round(ms / ms_single, 4)}
 
 
+def time_server(d: dict, dev: dict, n_slots: int, steps: int, warmup: int, ms_single: float):
+    """The batch spread over `n_slots` client slots of one layer, served by
+    eaas_server_step.  The step writes its results over the hidden states, so
+    before every step the clients' requests are posted again: the hidden
+    states are copied back into the payloads and all flags set ready (a copy
+    of T*H bf16 and a fill kernel, inside the timed loop)."""
+    import torch
+
+    from paper_2509_17863_amd import eaas
+
+    T, H, I, E, k = d["T"], d["H"], d["I"], d["E"], d["k"]
+    bounds = np.linspace(0, T, n_slots + 1).astype(int)
+    flags = torch.ones(n_slots, dtype=torch.int32, device="cuda")
+    hdr = torch.tensor([[0, b - a] for a, b in zip(bounds[:-1], bounds[1:])], dtype=torch.int32,
+                       device="cuda")
+    slots = [(flags[i:i + 1], hdr[i], dev["x"][a:b].clone(), dev["topk_ids"][a:b].clone(),
+              dev["topk_weights"][a:b].clone())
+             for i, (a, b) in enumerate(zip(bounds[:-1], bounds[1:]))]
+    stab = eaas.slot_table(slots)
+    ltab = eaas.layer_table([(dev["w_gate_up"], dev["w_gate_up_scale"], dev["w_down"],
+                              dev["w_down_scale"])])
+    wdt = eaas.EAAS_FP8_E4M3 if d["wdtype"] == "fp8" else eaas.EAAS_BF16
+    ws = eaas.alloc_server_workspace(T, H, I, E, k, 1, wdt)
+
+    def step():
+        for i, (a, b) in enumerate(zip(bounds[:-1], bounds[1:])):
+            slots[i][2].copy_(dev["x"][a:b])
+        flags.fill_(eaas.EAAS_SLOT_READY)
+        eaas.eaas_server_step(stab, n_slots, ltab, 1, T, H, I, E, k, ws, wdt)
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    done = int((flags == eaas.EAAS_SLOT_DONE).sum().item())
+    return {"entry": "eaas_server_step", "slots": n_slots, "slots_done_last_step": done,
+            "timed": "re-post of every request (payload copy, flags) + server step",
+            "ms_per_step": round(ms, 4), "value": round(T / (ms * 1e-3), 1), "unit": "tokens/s",
+            "vs_single_batch": round(ms / ms_single, 4)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -153,6 +197,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mixtral")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--server-slots", type=int, default=0,
+                    help="also time the server step over this many client slots holding the "
+                         "batch (flags set ready before every step)")
     ap.add_argument("--clients", type=int, default=0,
                     help="also time the dynamic-batch entry point with the batch split into "
                          "this many client requests (token counts read on the device)")
@@ -246,6 +293,8 @@ def main() -> int:
     }
     if args.clients > 0:
         res["segments"] = time_segments(d, dev, args.clients, args.steps, args.warmup, ms)
+    if args.server_slots > 0:
+        res["server_step"] = time_server(d, dev, args.server_slots, args.steps, args.warmup, ms)
     if hbm_bound:
         res["step_hbm_gbs"] = round((alg["gu_bytes"] + alg["dn_bytes"]) / (ms * 1e-3) / 1e9, 1)
     if not args.no_cpu_baseline:
