@@ -35,9 +35,11 @@
 // into LDS once and builds the per-expert M-tile prefix there.  Tile ids are
 // ordered expert-major, then in groups of 8 M-tiles, N-tile major and M-tile
 // minor inside a group, so tiles that run together share weight and token
-// tiles; workgroup ids are remapped so each XCD (ids congruent mod 8) gets a
-// contiguous range of tiles and its L2 sees that reuse.  The grid is sized for the worst case from R and E alone (no
-// host readback); surplus workgroups exit after the prologue.
+// tiles; workgroup ids are remapped so each XCD (ids congruent mod 8) runs 32
+// consecutive tiles at a time (its L2 sees that reuse) and the whole GPU one
+// window of 256 consecutive tiles (the MALL sees the re-reads across XCDs).
+// The grid is sized for the worst case from R and E alone (no host
+// readback); surplus workgroups exit after the prologue.
 #include <type_traits>
 
 #include "common.h"
@@ -180,9 +182,23 @@ __device__ __forceinline__ bool locate_tile(const GemmParams& p, int* s_tp, int*
   const int total = s_tp[n_active] * n_tiles_n;
   const int bid = blockIdx.x;
   if (bid >= total) return false;
+  // Workgroups are dispatched in id order and round-robin over the XCDs
+  // (XCD = id mod 8).  The k-th workgroup of XCD x takes tile
+  //   (k / 32) * 256 + x * 32 + k % 32,
+  // so the 32 workgroups an XCD runs at once hold 32 consecutive tiles (they
+  // share token and weight tiles in its L2) and the 256 running on the whole
+  // GPU hold one window of 256 consecutive tiles, which keeps the weights the
+  // XCDs re-read within the window in the shared MALL.  Tiles past the last
+  // whole window keep their ids.
   int tile = bid;
-  const int per = total / kNumXcd;
-  if (bid < per * kNumXcd) tile = (bid % kNumXcd) * per + bid / kNumXcd;
+  {
+    constexpr int kChunk = 32;
+    const int window = kNumXcd * kChunk;
+    if (bid < (total / window) * window) {
+      const int x = bid % kNumXcd, kk = bid / kNumXcd;
+      tile = (kk / kChunk) * window + x * kChunk + (kk % kChunk);
+    }
+  }
   int lo = 0, hi = n_active - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
