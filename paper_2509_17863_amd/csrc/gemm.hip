@@ -379,9 +379,9 @@ struct DmaLoop {
   static __device__ __forceinline__ int b_inst(int wave, int q) { return min(wave + NW * q, NB - 1); }
   static constexpr int INST = A_INST + B_INST;
   // LDS: a ring of SA token-row (A) stages, then a ring of SB weight (B)
-  // stages of BSPAN K tiles each.  SB = SA + 1 gives the weights, which come
-  // from HBM, one more K tile of flight time than the token rows, which
-  // mostly hit L2; BSPAN = 2 (with SA = SB = 2) gives them two.
+  // stages of BSPAN K tiles each.  SB > SA gives the weights, which stream
+  // from HBM, more K tiles of flight time than the token rows, which mostly
+  // hit L2; BSPAN = 2 (with SA = SB = 2) gives them two.
   static constexpr int A_BYTES = BM * RB;
   static constexpr int B_BYTES = BN * BRB;
   static constexpr int B_BASE = SA * A_BYTES;
@@ -389,7 +389,7 @@ struct DmaLoop {
   static constexpr int KK = BK / 16;           // MFMA k-steps per tile
   static constexpr int TILES_PER_SCALE = 128 / BK;  // fp8: K tiles per scale block
   static_assert(KK % 2 == 0, "fragment double buffering alternates sets");
-  static_assert(SA >= 2 && SB <= 4 && (SB == SA || (SB == SA + 1 && SA <= 3)), "ring depths");
+  static_assert(SA >= 2 && SB >= 2 && SA <= 4 && SB <= 4, "ring depths");
   static_assert(BSPAN == 1 || (BSPAN == 2 && FP8 && SA == 2 && SB == 2), "B stage span");
   static_assert(!FP8 || 128 % BK == 0, "fp8 scale blocks hold whole K tiles");
 
@@ -464,29 +464,36 @@ struct DmaLoop {
 
   // Wait until this wave's DMA of K tile kt+1 (both parts) has landed.  Loads
   // complete in issue order for vmcnt, so the wait allows exactly the
-  // instructions issued after the later of the two parts:
-  //   SA == SB: iteration i issues A(i+S-1) then B(i+S-1); after B(kt+1)
-  //     come the groups of tiles kt+2 .. kt+S-1 (those < nk).
-  //   SB == SA+1: iteration i issues A(i+SA-1) then B(i+SA); after A(kt+1)
-  //     come B(kt+2), then A(kt+2), B(kt+3) when SA == 3 (those < nk).
-  //   BSPAN == 2: iteration i issues A(i+1), then on even i B stage i/2+1;
-  //     after A(kt+1) comes that B stage when kt is even (B stage (kt+1)/2,
-  //     needed when kt is odd, was issued before A(kt)).
-  // kt = -1 is the prologue's wait for tile 0 (same issue order there).
+  // instructions issued after the later of the two parts.  Issue order:
+  // iteration i (tile i's first k-step) issues A(i+SA-1), then B(i+SB-1),
+  // each only if it exists; the prologue runs iterations -(max(SA,SB)-1) ..
+  // -1 the same way.  after_count(rem) counts, for a tile followed by `rem`
+  // more (3 stands for "3 or more": no ring looks further ahead), the
+  // instructions issued after the later of A(kt+1), B(kt+1) by the end of
+  // iteration kt.  BSPAN == 2: iteration i issues A(i+1), then on even i B
+  // stage i/2+1; after A(kt+1) comes that B stage when kt is even (B stage
+  // (kt+1)/2, needed when kt is odd, was issued before A(kt)).  kt = -1 is
+  // the prologue's wait for tile 0.
+  static constexpr int after_count(int rem) {
+    const int nk_rel = 1 + rem;                 // K tiles from kt on
+    const int j = 2 - (SA < SB ? SA : SB);      // iteration of the later part
+    int n = 0;
+    if (SA < SB && j + SB - 1 >= 0 && j + SB - 1 < nk_rel) n += B_INST;  // B after A(kt+1)
+    for (int i = j + 1; i <= 0; ++i) {
+      if (i + SA - 1 >= 0 && i + SA - 1 < nk_rel) n += A_INST;
+      if (i + SB - 1 >= 0 && i + SB - 1 < nk_rel) n += B_INST;
+    }
+    return n;
+  }
   static __device__ __forceinline__ void wait_next(int kt, int nk) {
     const int rem = nk - 1 - kt;  // K tiles from kt+1 on
     if constexpr (BSPAN == 2) {
       if (kt >= 0 && (kt & 1) == 0 && kt + 2 < nk) wait_vmcnt<B_INST>();
       else wait_vmcnt<0>();
-    } else if constexpr (SA == SB) {
-      if (SB > 3 && rem >= 3) wait_vmcnt<(SB > 3 ? 2 * INST : 0)>();
-      else if (SB > 2 && rem >= 2) wait_vmcnt<(SB > 2 ? INST : 0)>();
-      else wait_vmcnt<0>();
     } else {
-      if (SA == 3 && rem >= 3) wait_vmcnt<(SA == 3 ? INST + B_INST : 0)>();
-      else if (SA == 3 && rem >= 2) wait_vmcnt<(SA == 3 ? INST : 0)>();
-      else if (rem >= 2) wait_vmcnt<B_INST>();
-      else wait_vmcnt<0>();
+      if (rem >= 3) wait_vmcnt<after_count(3)>();
+      else if (rem == 2) wait_vmcnt<after_count(2)>();
+      else wait_vmcnt<after_count(1)>();
     }
   }
 
@@ -564,18 +571,12 @@ struct DmaLoop {
     if constexpr (BSPAN == 2) {
       issue_b(s, 0, nb);
       issue_a(s, 0, nk);
-    } else if constexpr (SA == SB) {
-#pragma unroll
-      for (int t = 0; t < SA - 1; ++t) {
-        issue_a(s, t, nk);
-        issue_b(s, t, nb);
-      }
     } else {
-      issue_b(s, 0, nb);
+      constexpr int S = SA > SB ? SA : SB;
 #pragma unroll
-      for (int t = 0; t < SA - 1; ++t) {
-        issue_a(s, t, nk);
-        issue_b(s, t + 1, nb);
+      for (int i = -(S - 1); i <= -1; ++i) {
+        if (i + SA - 1 >= 0) issue_a(s, i + SA - 1, nk);
+        if (i + SB - 1 >= 0) issue_b(s, i + SB - 1, nb);
       }
     }
     wait_next(-1, nk);
@@ -1129,15 +1130,15 @@ hipError_t launch_pp(const GemmParams& p, int R, int E, hipStream_t stream) {
 //   fp8 weights: 96x512 tiles (a decode batch's ~50-90 rows per expert fit
 //     one tile, so the weights stream once), 8 waves of 96x64 -- two per
 //     SIMD, so one wave's partial-sum scaling (VALU) overlaps the other's
-//     MFMAs -- BK=64, 3 stages so 64 KiB of weights per CU are in flight
-//     while a tile is multiplied (96x256 with 4 waves when N is not a
-//     multiple of 512);
+//     MFMAs -- BK=64, 2 token-row stages and 4 weight stages (152 KiB), so
+//     96 KiB of weights per CU are in flight while a tile is multiplied
+//     (96x256 with 4 waves and 3+3 stages when N is not a multiple of 512);
 //   decode-sized bf16 and other N: register-staged 128-row tiles.
 template <int KIND, bool FP8>
 hipError_t launch_kind(const GemmParams& p, int R, int E, bool small_m, hipStream_t stream) {
   const bool n256 = (p.N % 256) == 0;
   if constexpr (FP8) {
-    if (p.N % 512 == 0) return launch_dma<KIND, true, 64, 3, 3, 1, 1, 8, 3, 2>(p, R, E, stream);
+    if (p.N % 512 == 0) return launch_dma<KIND, true, 64, 2, 4, 1, 1, 8, 3, 2>(p, R, E, stream);
     if (n256) return launch_dma<KIND, true, 64, 3, 3, 1, 1, 4, 3, 2>(p, R, E, stream);
     if (small_m) return launch_reg<KIND, true, 1, 2, 4, 2>(p, R, E, stream);
     return launch_reg<KIND, true, 2, 2, 4, 2>(p, R, E, stream);
