@@ -109,6 +109,29 @@ def cpu_baseline(d: dict, target_s: float = 12.0) -> dict:
                       f"sub-batch, fp64 BLAS, {t:.1f} s; weights converted to fp64 beforehand)"}
 
 
+def time_graph(step, steps: int, warmup: int) -> float:
+    """ms per step of `step` captured once in a graph and replayed."""
+    import torch
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.replay()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
 def time_segments(d: dict, dev: dict, clients: int, steps: int, warmup: int, ms_single: float):
     """The same batch as `clients` requests in separate buffers, through
     eaas_expert_forward_segments (counts on the device, capacity T)."""
@@ -257,6 +280,10 @@ def main() -> int:
     def mean_ms(a, b):
         return float(np.mean([evs[i][a].elapsed_time(evs[i][b]) for i in range(args.steps)]))
 
+    # the step as the paper deploys it (§4.3): captured once in a graph, then
+    # replayed; the same kernels with no launches from the host per step
+    ms_graph = time_graph(step, args.steps, args.warmup)
+
     t_route, t_gu, t_dn, t_comb = mean_ms(0, 1), mean_ms(1, 2), mean_ms(2, 3), mean_ms(3, 4)
     t_step_ev = mean_ms(0, 4)
     hbm_bound = d["wdtype"] == "fp8"
@@ -274,17 +301,21 @@ def main() -> int:
     roof["kernel"] = gate_up_kernel_name(d)
     res = {
         "metric": "expert-FFN tokens/s",
-        "value": round(T / (ms * 1e-3), 1),
+        "value": round(T / (ms_graph * 1e-3), 1),
         "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms, 4),
+        "ms_per_step": round(ms_graph, 4),
+        "timing": "hipGraph replay of eaas_expert_forward (per-kernel times from an eager pass "
+                  "with events in the same run)",
+        "eager": {"ms_per_step": round(ms, 4), "value": round(T / (ms * 1e-3), 1),
+                  "graph_speedup": round(ms / ms_graph, 4)},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": args.workload, "T": T, "H": H, "I": I, "E": E, "k": k,
                    "weights": d["wdtype"], "seed": wl.seed, "zipf": wl.zipf,
                    "active_experts": int((counts > 0).sum()), "parallelism": "none (1 GPU)"},
-        "step_tflops": round(alg["flops"] / (ms * 1e-3) / 1e12, 1),
-        "step_frac_bf16_peak": round(alg["flops"] / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "step_tflops": round(alg["flops"] / (ms_graph * 1e-3) / 1e12, 1),
+        "step_frac_bf16_peak": round(alg["flops"] / (ms_graph * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "kernels_ms": {"route": round(t_route, 4), "gate_up": round(t_gu, 4),
                        "down": round(t_dn, 4), "combine": round(t_comb, 4),
                        "step_events": round(t_step_ev, 4)},
@@ -296,7 +327,7 @@ def main() -> int:
     if args.server_slots > 0:
         res["server_step"] = time_server(d, dev, args.server_slots, args.steps, args.warmup, ms)
     if hbm_bound:
-        res["step_hbm_gbs"] = round((alg["gu_bytes"] + alg["dn_bytes"]) / (ms * 1e-3) / 1e9, 1)
+        res["step_hbm_gbs"] = round((alg["gu_bytes"] + alg["dn_bytes"]) / (ms_graph * 1e-3) / 1e9, 1)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(d)
     print(json.dumps(res), flush=True)
