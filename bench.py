@@ -109,8 +109,10 @@ def cpu_baseline(d: dict, target_s: float = 12.0) -> dict:
                       f"sub-batch, fp64 BLAS, {t:.1f} s; weights converted to fp64 beforehand)"}
 
 
-def time_graph(step, steps: int, warmup: int) -> float:
-    """ms per step of `step` captured once in a graph and replayed."""
+def time_graph(step, steps: int, warmup: int) -> tuple[float, dict]:
+    """ms per step of `step` captured once in a graph and replayed (wall clock
+    over all replays), and the median / p10 / p90 of the replays' event times
+    (a second pass, each replay bracketed by events on the replay stream)."""
     import torch
 
     side = torch.cuda.Stream()
@@ -129,7 +131,40 @@ def time_graph(step, steps: int, warmup: int) -> float:
     for _ in range(steps):
         g.replay()
     torch.cuda.synchronize()
-    return (time.perf_counter() - t0) * 1e3 / steps
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    cur = torch.cuda.current_stream()
+    for a, b in ev:
+        a.record(cur)
+        g.replay()
+        b.record(cur)
+    torch.cuda.synchronize()
+    t = np.array([a.elapsed_time(b) for a, b in ev])
+    return ms, {"median": round(float(np.median(t)), 4), "p10": round(float(np.percentile(t, 10)), 4),
+                "p90": round(float(np.percentile(t, 90)), 4)}
+
+
+def gpu_clocks() -> dict | None:
+    """Current engine (sclk) and memory (mclk) clock levels of the first GPU
+    from sysfs (the level marked '*'); None where the files are absent."""
+    import glob
+
+    out = {}
+    for dev in sorted(glob.glob("/sys/class/drm/card*/device")):
+        for name in ("pp_dpm_sclk", "pp_dpm_mclk", "pp_dpm_fclk"):
+            try:
+                with open(os.path.join(dev, name)) as fh:
+                    for line in fh:
+                        if "*" in line:
+                            m = re.search(r"(\d+)\s*[Mm]hz", line)
+                            if m:
+                                out[name[-4:]] = int(m.group(1))
+            except OSError:
+                pass
+        if out:
+            return out
+    return None
 
 
 def time_segments(d: dict, dev: dict, clients: int, steps: int, warmup: int, ms_single: float):
@@ -264,6 +299,7 @@ def main() -> int:
                                               dev["w_gate_up_scale"], dev["w_down_scale"],
                                               events=ev)
 
+    clocks_before = gpu_clocks()
     for ev in evs:  # create the events before the timed region
         for e in ev:
             e.record(stream)
@@ -282,7 +318,8 @@ def main() -> int:
 
     # the step as the paper deploys it (§4.3): captured once in a graph, then
     # replayed; the same kernels with no launches from the host per step
-    ms_graph = time_graph(step, args.steps, args.warmup)
+    ms_graph, graph_stats = time_graph(step, args.steps, args.warmup)
+    clocks_after = gpu_clocks()
 
     t_route, t_gu, t_dn, t_comb = mean_ms(0, 1), mean_ms(1, 2), mean_ms(2, 3), mean_ms(3, 4)
     t_step_ev = mean_ms(0, 4)
@@ -307,6 +344,7 @@ def main() -> int:
         "ms_per_step": round(ms_graph, 4),
         "timing": "hipGraph replay of eaas_expert_forward (per-kernel times from an eager pass "
                   "with events in the same run)",
+        "graph_replay_ms": graph_stats,
         "eager": {"ms_per_step": round(ms, 4), "value": round(T / (ms * 1e-3), 1),
                   "graph_speedup": round(ms / ms_graph, 4)},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
@@ -316,6 +354,9 @@ def main() -> int:
                    "active_experts": int((counts > 0).sum()), "parallelism": "none (1 GPU)"},
         "step_tflops": round(alg["flops"] / (ms_graph * 1e-3) / 1e12, 1),
         "step_frac_bf16_peak": round(alg["flops"] / (ms_graph * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        # the two grouped GEMMs alone: 6RHI over their summed event times
+        "gemm_tflops": round(alg["flops"] / ((t_gu + t_dn) * 1e-3) / 1e12, 1),
+        "gemm_frac_bf16_peak": round(alg["flops"] / ((t_gu + t_dn) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "kernels_ms": {"route": round(t_route, 4), "gate_up": round(t_gu, 4),
                        "down": round(t_dn, 4), "combine": round(t_comb, 4),
                        "step_events": round(t_step_ev, 4)},
@@ -324,6 +365,7 @@ def main() -> int:
     }
     if args.clients > 0:
         res["segments"] = time_segments(d, dev, args.clients, args.steps, args.warmup, ms)
+    res["clocks_mhz"] = {"before": clocks_before, "after": clocks_after}
     if args.server_slots > 0:
         res["server_step"] = time_server(d, dev, args.server_slots, args.steps, args.warmup, ms)
     if hbm_bound:
