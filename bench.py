@@ -20,6 +20,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 
@@ -47,6 +48,8 @@ def algorithmic(d: dict, counts: np.ndarray) -> dict:
 def gate_up_kernel_name(d: dict) -> str:
     """The gate/up kernel the library dispatches for this workload's shape."""
     T, I, E, k = d["T"], d["I"], d["E"], d["k"]
+    if d.get("act8"):
+        return "grouped_gemm_w8a8_kernel<gate/up>"
     if d["wdtype"] == "fp8":
         return "grouped_gemm_dma_kernel<gate/up, fp8 weights>"
     if T * k <= 128 * E or (2 * I) % 256:
@@ -84,6 +87,9 @@ def cpu_baseline(d: dict, target_s: float = 12.0) -> dict:
     to fp64 outside the timed region)."""
     from oracle import eaas_oracle as O
 
+    if d.get("act8"):
+        return cpu_baseline_w8a8(d, target_s)
+
     E = d["E"]
     w64 = ([], [])
     for e in range(E):
@@ -107,6 +113,32 @@ def cpu_baseline(d: dict, target_s: float = 12.0) -> dict:
     return {"value": n / t, "unit": "tokens/s", "cores": cpu_threads(), "kind": "oracle",
             "sample": f"{n} of {d['T']} tokens of the same batch (oracle expert_forward on the "
                       f"sub-batch, fp64 BLAS, {t:.1f} s; weights converted to fp64 beforehand)"}
+
+
+def cpu_baseline_w8a8(d: dict, target_s: float = 12.0) -> dict:
+    """The fp8-activation oracle, untuned, on a bounded token sample (it
+    dequantizes each active expert's weights inside the timed region)."""
+    from oracle import eaas_oracle as O
+    from oracle import w8a8_oracle as W
+
+    rng = np.random.default_rng(7)
+
+    def run(n):
+        tok = np.sort(rng.choice(d["T"], size=n, replace=False))
+        sub = O.sub_batch(d, tok)
+        t0 = time.perf_counter()
+        W.expert_forward_w8a8(sub)
+        return time.perf_counter() - t0
+
+    n = min(d["T"], 64)
+    t = run(n)
+    if t < target_s and n < d["T"]:
+        n = int(min(d["T"], max(n, n * target_s / max(t, 1e-3))))
+        t = run(n)
+    return {"value": n / t, "unit": "tokens/s", "cores": cpu_threads(), "kind": "oracle",
+            "sample": f"{n} of {d['T']} tokens of the same batch (fp8-activation oracle on the "
+                      f"sub-batch, fp64 BLAS, {t:.1f} s including the per-expert weight "
+                      "dequantization)"}
 
 
 def time_graph(step, steps: int, warmup: int) -> tuple[float, dict]:
@@ -183,7 +215,9 @@ def time_segments(d: dict, dev: dict, clients: int, steps: int, warmup: int, ms_
                      torch.empty((max(b - a, 1), H), dtype=torch.bfloat16, device="cuda")))
     table = eaas.segment_table(bufs)
     counts = torch.tensor(np.diff(bounds), dtype=torch.int32, device="cuda")
-    wdt = eaas.EAAS_FP8_E4M3 if d["wdtype"] == "fp8" else eaas.EAAS_BF16
+    act8 = bool(d.get("act8"))
+    wdt = (eaas.EAAS_FP8_E4M3_A8 if act8 else eaas.EAAS_FP8_E4M3) if d["wdtype"] == "fp8" \
+        else eaas.EAAS_BF16
     ws = eaas.alloc_segments_workspace(T, H, I, E, k, wdt)
 
     def step():
@@ -225,7 +259,9 @@ def time_server(d: dict, dev: dict, n_slots: int, steps: int, warmup: int, ms_si
     stab = eaas.slot_table(slots)
     ltab = eaas.layer_table([(dev["w_gate_up"], dev["w_gate_up_scale"], dev["w_down"],
                               dev["w_down_scale"])])
-    wdt = eaas.EAAS_FP8_E4M3 if d["wdtype"] == "fp8" else eaas.EAAS_BF16
+    act8 = bool(d.get("act8"))
+    wdt = (eaas.EAAS_FP8_E4M3_A8 if act8 else eaas.EAAS_FP8_E4M3) if d["wdtype"] == "fp8" \
+        else eaas.EAAS_BF16
     ws = eaas.alloc_server_workspace(T, H, I, E, k, 1, wdt)
 
     def step():
@@ -279,7 +315,9 @@ def main() -> int:
     d = synth.make_workload(args.workload)
     dev = to_device(d)
     T, H, I, E, k = d["T"], d["H"], d["I"], d["E"], d["k"]
-    wdt = eaas.EAAS_FP8_E4M3 if d["wdtype"] == "fp8" else eaas.EAAS_BF16
+    act8 = bool(d.get("act8"))
+    wdt = (eaas.EAAS_FP8_E4M3_A8 if act8 else eaas.EAAS_FP8_E4M3) if d["wdtype"] == "fp8" \
+        else eaas.EAAS_BF16
     ws = eaas.alloc_workspace(T, H, I, E, k, wdt)
     out = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
     counts = np.bincount(d["topk_ids"].ravel()[d["topk_ids"].ravel() >= 0], minlength=E)
@@ -292,12 +330,12 @@ def main() -> int:
         if ev is None:
             eaas.eaas_expert_forward(dev["x"], dev["topk_ids"], dev["topk_weights"],
                                      dev["w_gate_up"], dev["w_down"], out, ws,
-                                     dev["w_gate_up_scale"], dev["w_down_scale"])
+                                     dev["w_gate_up_scale"], dev["w_down_scale"], act8=act8)
         else:
             eaas.eaas_expert_forward_profiled(dev["x"], dev["topk_ids"], dev["topk_weights"],
                                               dev["w_gate_up"], dev["w_down"], out, ws,
                                               dev["w_gate_up_scale"], dev["w_down_scale"],
-                                              events=ev)
+                                              events=ev, act8=act8)
 
     clocks_before = gpu_clocks()
     for ev in evs:  # create the events before the timed region
@@ -323,8 +361,13 @@ def main() -> int:
 
     t_route, t_gu, t_dn, t_comb = mean_ms(0, 1), mean_ms(1, 2), mean_ms(2, 3), mean_ms(3, 4)
     t_step_ev = mean_ms(0, 4)
-    hbm_bound = d["wdtype"] == "fp8"
-    if hbm_bound:
+    hbm_bound = d["wdtype"] == "fp8" and not act8
+    if act8:
+        # fp8 x fp8 contraction: priced against the fp8 MFMA peak
+        achieved = alg["gu_flops"] / (t_gu * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_FP8_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP8_TFLOPS, 4), "traffic": None}
+    elif hbm_bound:
         achieved = alg["gu_bytes"] / (t_gu * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
@@ -348,7 +391,7 @@ def main() -> int:
         "eager": {"ms_per_step": round(ms, 4), "value": round(T / (ms * 1e-3), 1),
                   "graph_speedup": round(ms / ms_graph, 4)},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic",
+        "dtype": "fp8e4m3" if act8 else "bf16", "data": "synthetic",
         "config": {"workload": args.workload, "T": T, "H": H, "I": I, "E": E, "k": k,
                    "weights": d["wdtype"], "seed": wl.seed, "zipf": wl.zipf,
                    "active_experts": int((counts > 0).sum()), "parallelism": "none (1 GPU)"},

@@ -76,7 +76,17 @@ enum eaas_status {
 enum eaas_dtype {
   EAAS_BF16 = 0,     /* bfloat16 bit patterns (uint16)                    */
   EAAS_FP8_E4M3 = 1, /* OCP fp8 e4m3fn bit patterns (uint8), weights only */
-  EAAS_FP32 = 2      /* IEEE binary32, outputs only                       */
+  EAAS_FP32 = 2,     /* IEEE binary32, outputs only                       */
+  /* As a weight dtype: fp8 e4m3fn weights (as EAAS_FP8_E4M3) and fp8
+   * activations.  The step quantizes x per token and h per row, per block of
+   * 128 channels (s = amax/448, 1 for an all-zero block; q = e4m3(a/s),
+   * nearest even, saturating at 448; fp32 arithmetic), and runs both grouped
+   * GEMMs on fp8 x fp8 MFMAs with fp32 accumulation, scaling each 128-wide K
+   * block's partial sums by its row scale times its weight block scale (the
+   * block-scaled fp8 GEMM of the grouped-GEMM engine named in §4.1).  Needs
+   * H a multiple of 256.  Accepted by eaas_workspace_bytes,
+   * eaas_expert_ffn_grouped, eaas_expert_forward(_profiled). */
+  EAAS_FP8_E4M3_A8 = 3
 };
 
 /*
@@ -103,6 +113,37 @@ typedef struct eaas_routing {
  * weight dtype (the maximum over the entry points).  Returns 0 for a shape the
  * library rejects. */
 size_t eaas_workspace_bytes(const eaas_shape *s, int w_dtype);
+
+/* Where a forward call leaves its intermediates inside the workspace (for
+ * inspection and tests; the contents are those of the last call that used
+ * the workspace, rows in the grouped order of the routing):
+ *   EAAS_WS_H      h [R,I] bf16 (bf16 and fp8-weight modes)
+ *   EAAS_WS_HQ     h quantized [R,I] e4m3fn codes   (EAAS_FP8_E4M3_A8)
+ *   EAAS_WS_HS     its scales [R,I/128] fp32         (EAAS_FP8_E4M3_A8)
+ *   EAAS_WS_XQ     x quantized [T,H] e4m3fn codes    (EAAS_FP8_E4M3_A8)
+ *   EAAS_WS_XS     its scales [T,H/128] fp32         (EAAS_FP8_E4M3_A8)
+ *   EAAS_WS_STAGE  weighted expert outputs [R,H] fp32, row = slot
+ *                  t*k+j (eaas_expert_forward; invalid slots untouched)
+ * Writes the byte offset and size of the region.  Returns INVALID_ARG for a
+ * null output pointer, an unknown region or one the dtype does not have,
+ * UNSUPPORTED for a shape or dtype eaas_workspace_bytes rejects. */
+enum eaas_ws_region {
+  EAAS_WS_H = 0, EAAS_WS_HQ = 1, EAAS_WS_HS = 2, EAAS_WS_XQ = 3, EAAS_WS_XS = 4,
+  EAAS_WS_STAGE = 5
+};
+int eaas_workspace_region(const eaas_shape *s, int w_dtype, int region, size_t *offset,
+                          size_t *bytes);
+
+/* Activation quantization of the EAAS_FP8_E4M3_A8 step, on its own:
+ *   x [rows,K] bf16 (device), K a multiple of 128 and rows*K < 2^31
+ *   q [rows,K] e4m3fn codes (device, written), s [rows,K/128] fp32 (device,
+ *   written): per row and block of 128 channels, s = amax/448 (1 if the block
+ *   is all zero), q = e4m3fn(x/s) rounded to nearest even and saturated at
+ *   +-448, with s and x/s correctly rounded fp32.
+ * x, q 16-byte aligned.  rows == 0 is a no-op.  Errors: INVALID_ARG (null or
+ * misaligned pointer, rows < 0, K <= 0), UNSUPPORTED (K % 128, size), HIP. */
+int eaas_quantize_rows_fp8(const void *x, int64_t rows, int32_t K, void *q, float *s,
+                           void *stream);
 
 /* Token reorganisation + group-shrink (§3.3 Fig. 5, §4.1).
  *   topk_ids [T,k] int32   expert id per slot (payload `expert_id`, §3.2)

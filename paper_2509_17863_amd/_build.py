@@ -11,7 +11,7 @@ PKG = Path(__file__).resolve().parent
 CSRC = PKG / "csrc"
 BUILD = PKG / "_build"
 LIB = PKG / "libeaas.so"
-SOURCES = ["route.hip", "gemm.hip", "combine.hip", "segments.hip", "eaas_api.hip"]
+SOURCES = ["route.hip", "gemm.hip", "combine.hip", "segments.hip", "quant.hip", "eaas_api.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

@@ -28,6 +28,18 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
 }
 
+// fp32 -> OCP fp8 e4m3fn: round to nearest even, magnitudes past 448
+// saturated to 448 (NaN passes through to a NaN code).  Four values packed
+// into one word, the first in the low byte.
+__device__ __forceinline__ float clamp_e4m3(float v) {
+  return fabsf(v) > 448.0f ? copysignf(448.0f, v) : v;
+}
+
+__device__ __forceinline__ uint32_t pack_e4m3x4(float a, float b, float c, float d) {
+  uint32_t w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(clamp_e4m3(a), clamp_e4m3(b), 0, false);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(clamp_e4m3(c), clamp_e4m3(d), (int)w, true);
+}
+
 // Lane mask of lanes below the caller in the wave.
 __device__ __forceinline__ uint64_t lanemask_lt() {
   const int lane = __lane_id();

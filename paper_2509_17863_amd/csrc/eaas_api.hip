@@ -4,6 +4,8 @@
 #include <limits.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "internal.h"
 
@@ -17,11 +19,14 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 struct WsLayout {
   size_t hist, counts, offsets, perm, inv, active, h, stage, total;
+  // fp8 activations: h held as hq [R,I] + hs [R,I/128] inside the h region,
+  // x quantized into xq [T,H] + xs [T,H/128] after the staging
+  size_t hq, hs, xq, xs;
   // dynamic batch only: the requests gathered into one contiguous batch
   size_t x_cat, ids_cat, w_cat, seg_total;
 };
 
-WsLayout layout(const eaas_shape& s) {
+WsLayout layout(const eaas_shape& s, int w_dtype = EAAS_BF16) {
   const size_t R = (size_t)s.T * s.k;
   WsLayout L{};
   size_t o = 0;
@@ -31,8 +36,15 @@ WsLayout layout(const eaas_shape& s) {
   L.perm = o;    o = align_up(o + R * 4);
   L.inv = o;     o = align_up(o + R * 4);
   L.active = o;  o = align_up(o + (size_t)(s.E + 1) * 4);
-  L.h = o;       o = align_up(o + R * s.I * 2);
+  L.h = o;
+  L.hq = L.h;
+  L.hs = align_up(L.h + R * s.I);
+  o = align_up(std::max(L.h + R * s.I * 2, L.hs + R * (s.I / 128) * 4));
   L.stage = o;   o = align_up(o + R * s.H * 4);
+  if (w_dtype == EAAS_FP8_E4M3_A8) {
+    L.xq = o;    o = align_up(o + (size_t)s.T * s.H);
+    L.xs = o;    o = align_up(o + (size_t)s.T * (s.H / 128) * 4);
+  }
   L.total = o;
   L.x_cat = o;   o = align_up(o + (size_t)s.T * s.H * 2);
   L.ids_cat = o; o = align_up(o + R * 4);
@@ -63,8 +75,34 @@ bool routing_ok(const eaas_routing* r) {
 bool weights_ok(const void* wgu, const float* sgu, const void* wd, const float* sd, int w_dtype) {
   if (!wgu || !wd || !aligned16(wgu) || !aligned16(wd)) return false;
   if (w_dtype == EAAS_BF16) return true;
-  if (w_dtype == EAAS_FP8_E4M3) return sgu && sd;
+  if (w_dtype == EAAS_FP8_E4M3 || w_dtype == EAAS_FP8_E4M3_A8) return sgu && sd;
   return false;
+}
+
+// Shape limits of a weight dtype beyond check_shape (fp8 activations: the
+// down projection's N = H in 256-wide tiles).
+int check_dtype_shape(const eaas_shape* s, int w_dtype) {
+  if (w_dtype == EAAS_FP8_E4M3_A8 && s->H % 256) return EAAS_ERR_UNSUPPORTED;
+  return EAAS_OK;
+}
+
+// FfnArgs members of the weight dtype (h and y are set by the caller).
+void set_dtype_args(FfnArgs& a, int w_dtype, char* base, const WsLayout& L) {
+  a.fp8 = w_dtype == EAAS_FP8_E4M3 || w_dtype == EAAS_FP8_E4M3_A8;
+  a.act8 = w_dtype == EAAS_FP8_E4M3_A8;
+  if (a.act8) {
+    a.xq = reinterpret_cast<const uint8_t*>(base + L.xq);
+    a.xs = reinterpret_cast<const float*>(base + L.xs);
+    a.hq = reinterpret_cast<uint8_t*>(base + L.hq);
+    a.hs = reinterpret_cast<float*>(base + L.hs);
+  }
+}
+
+// fp8 activations: quantize x into the workspace before the gate/up GEMM.
+hipError_t quantize_x(const FfnArgs& a, char* base, const WsLayout& L, hipStream_t hs) {
+  if (!a.act8) return hipSuccess;
+  return launch_quantize_rows(a.x, a.T, a.H, reinterpret_cast<uint8_t*>(base + L.xq),
+                              reinterpret_cast<float*>(base + L.xs), hs);
 }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? EAAS_OK : EAAS_ERR_HIP; }
@@ -85,8 +123,50 @@ extern "C" {
 
 size_t eaas_workspace_bytes(const eaas_shape* s, int w_dtype) {
   if (check_shape(s) != EAAS_OK) return 0;
-  if (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3) return 0;
-  return layout(*s).total;
+  if (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3 && w_dtype != EAAS_FP8_E4M3_A8) return 0;
+  if (check_dtype_shape(s, w_dtype) != EAAS_OK) return 0;
+  return layout(*s, w_dtype).total;
+}
+
+int eaas_workspace_region(const eaas_shape* s, int w_dtype, int region, size_t* offset,
+                          size_t* bytes) {
+  if (!offset || !bytes) return EAAS_ERR_INVALID_ARG;
+  if (eaas_workspace_bytes(s, w_dtype) == 0) return EAAS_ERR_UNSUPPORTED;
+  const WsLayout L = layout(*s, w_dtype);
+  const size_t R = (size_t)s->T * s->k;
+  const bool a8 = w_dtype == EAAS_FP8_E4M3_A8;
+  switch (region) {
+    case EAAS_WS_H:
+      if (a8) return EAAS_ERR_INVALID_ARG;
+      *offset = L.h; *bytes = R * s->I * 2; return EAAS_OK;
+    case EAAS_WS_HQ:
+      if (!a8) return EAAS_ERR_INVALID_ARG;
+      *offset = L.hq; *bytes = R * s->I; return EAAS_OK;
+    case EAAS_WS_HS:
+      if (!a8) return EAAS_ERR_INVALID_ARG;
+      *offset = L.hs; *bytes = R * (s->I / 128) * 4; return EAAS_OK;
+    case EAAS_WS_XQ:
+      if (!a8) return EAAS_ERR_INVALID_ARG;
+      *offset = L.xq; *bytes = (size_t)s->T * s->H; return EAAS_OK;
+    case EAAS_WS_XS:
+      if (!a8) return EAAS_ERR_INVALID_ARG;
+      *offset = L.xs; *bytes = (size_t)s->T * (s->H / 128) * 4; return EAAS_OK;
+    case EAAS_WS_STAGE:
+      *offset = L.stage; *bytes = R * s->H * 4; return EAAS_OK;
+    default:
+      return EAAS_ERR_INVALID_ARG;
+  }
+}
+
+int eaas_quantize_rows_fp8(const void* x, int64_t rows, int32_t K, void* q, float* s,
+                           void* stream) {
+  if (rows < 0 || K <= 0) return EAAS_ERR_INVALID_ARG;
+  if (K % 128 || rows * (int64_t)K > INT_MAX) return EAAS_ERR_UNSUPPORTED;
+  if (rows == 0) return EAAS_OK;
+  if (!x || !q || !s || !aligned16(x) || !aligned16(q)) return EAAS_ERR_INVALID_ARG;
+  return hip_status(launch_quantize_rows(static_cast<const uint16_t*>(x), rows, K,
+                                         static_cast<uint8_t*>(q), s,
+                                         reinterpret_cast<hipStream_t>(stream)));
 }
 
 int eaas_route_permute(const eaas_shape* s, const int32_t* topk_ids, const eaas_routing* r,
@@ -113,7 +193,8 @@ int eaas_expert_ffn_grouped(const eaas_shape* s, const void* x, const eaas_routi
   if (!x || !aligned16(x) || !routing_ok(r) || !y_perm || !aligned16(y_perm) ||
       !weights_ok(w_gate_up, w_gate_up_scale, w_down, w_down_scale, w_dtype))
     return EAAS_ERR_INVALID_ARG;
-  const WsLayout L = layout(*s);
+  if ((st = check_dtype_shape(s, w_dtype)) != EAAS_OK) return st;
+  const WsLayout L = layout(*s, w_dtype);
   if (!ws || !aligned16(ws) || ws_bytes < L.total) return EAAS_ERR_WORKSPACE;
   char* base = static_cast<char*>(ws);
   FfnArgs a{};
@@ -126,13 +207,14 @@ int eaas_expert_ffn_grouped(const eaas_shape* s, const void* x, const eaas_routi
   a.s_gate_up = w_gate_up_scale;
   a.w_down = w_down;
   a.s_down = w_down_scale;
-  a.fp8 = w_dtype == EAAS_FP8_E4M3;
+  set_dtype_args(a, w_dtype, base, L);
   a.h = reinterpret_cast<uint16_t*>(base + L.h);
   a.y = y_perm;
   a.topk_weights = nullptr;
   a.epilogue = kDownPlain;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = launch_gate_up(a, hs);
+  hipError_t e = quantize_x(a, base, L, hs);
+  if (e == hipSuccess) e = launch_gate_up(a, hs);
   if (e == hipSuccess) e = launch_down(a, hs);
   return hip_status(e);
 }
@@ -172,7 +254,8 @@ int eaas_expert_forward_profiled(const eaas_shape* s, const void* x, const int32
   } else if (op < xp + xb && xp < op + ob) {
     return EAAS_ERR_INVALID_ARG;
   }
-  const WsLayout L = layout(*s);
+  if ((st = check_dtype_shape(s, w_dtype)) != EAAS_OK) return st;
+  const WsLayout L = layout(*s, w_dtype);
   if (!ws || !aligned16(ws) || ws_bytes < L.total) return EAAS_ERR_WORKSPACE;
   char* base = static_cast<char*>(ws);
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
@@ -196,12 +279,15 @@ int eaas_expert_forward_profiled(const eaas_shape* s, const void* x, const int32
   a.s_gate_up = w_gate_up_scale;
   a.w_down = w_down;
   a.s_down = w_down_scale;
-  a.fp8 = w_dtype == EAAS_FP8_E4M3;
+  set_dtype_args(a, w_dtype, base, L);
   a.h = reinterpret_cast<uint16_t*>(base + L.h);
   a.y = stage;
   a.topk_weights = topk_weights;
   a.epilogue = kDownWeighted;
-  if (mark(1) != hipSuccess) return EAAS_ERR_HIP;
+  // (fp8 activations: x is quantized in the routing interval, so the gate/up
+  // interval times the GEMM alone)
+  e = quantize_x(a, base, L, hs);
+  if (e != hipSuccess || mark(1) != hipSuccess) return EAAS_ERR_HIP;
   e = launch_gate_up(a, hs);
   if (e != hipSuccess || mark(2) != hipSuccess) return EAAS_ERR_HIP;
   e = launch_down(a, hs);
@@ -235,6 +321,7 @@ int eaas_expert_forward_segments(const eaas_shape* s, const eaas_segment* segs,
                                  size_t ws_bytes, void* stream) {
   int st = check_shape(s);
   if (st != EAAS_OK) return st;
+  if (w_dtype == EAAS_FP8_E4M3_A8) return EAAS_ERR_UNSUPPORTED;  // single-batch entry points only
   if (n_seg < 0 || n_seg > kMaxSegments) return EAAS_ERR_INVALID_ARG;
   if (s->T == 0 || n_seg == 0) return EAAS_OK;
   if (!segs || !num_tokens || (out_dtype != EAAS_BF16 && out_dtype != EAAS_FP32) ||
@@ -328,6 +415,7 @@ int eaas_server_step(const eaas_shape* s, const eaas_slot* slots, int n_slots,
   eaas_shape g;
   int st = server_shape(s, n_layers, &g);
   if (st != EAAS_OK) return st;
+  if (w_dtype == EAAS_FP8_E4M3_A8) return EAAS_ERR_UNSUPPORTED;  // single-batch entry points only
   if (n_slots < 0 || n_slots > kMaxSegments) return EAAS_ERR_INVALID_ARG;
   if (n_slots == 0) return EAAS_OK;
   if (!slots || !layers || (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3))

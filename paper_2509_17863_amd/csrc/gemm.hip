@@ -78,6 +78,13 @@ struct GemmParams {
   const eaas_layer_weights* layers;  // nullptr: one weight array (b, b_scale)
   int e_layer;
   bool down;              // the records' down-projection members
+  // fp8 activations: A is fp8 (a8, rows of K bytes) with one fp32 scale per
+  // row and 128 channels (a_scale [rows, K/128]); the gate/up epilogue writes
+  // h quantized the same way (hq [R, I], hs [R, I/128])
+  const uint8_t* a8;
+  const float* a_scale;
+  uint8_t* hq;
+  float* hs;
 };
 
 // Weights of group e ([N, K], bf16 or fp8 bytes of esz each).
@@ -1125,6 +1132,264 @@ hipError_t launch_pp(const GemmParams& p, int R, int E, hipStream_t stream) {
   return hipGetLastError();
 }
 
+
+// ============================================================================
+// fp8 weights x fp8 activations
+// ============================================================================
+// Both operands are e4m3fn with fp32 scales: the weights one per 128x128
+// block, the activations one per row and 128 channels.  A K tile is 128
+// channels, exactly one scale block of both, and 128 bytes per LDS row as in
+// the bf16 loops (same DMA geometry and swizzle).  The block-scaled MFMA
+// (v_mfma_scale_f32_32x32x64_f8f6f4, unit block scales) takes 32 bytes of K
+// per lane; A and B fragments hold the same K bytes in the same order, so the
+// two MFMAs of a 32x32 block per K tile give that tile's fp32 dot products
+// in `part`, and then acc += (row scale * weight block scale) * part.
+// 8 waves of 64x64 (2x2 blocks of 32x32) over a 128x256 tile; a 3-stage
+// ring holds each K tile's token rows, their row scales and the weight rows.
+// The gate/up epilogue quantizes h per row over the tile's 128 h columns (the
+// 4 column waves combine their row maxima in LDS).
+namespace w8 {
+constexpr int BM = 128, BN = 256, NT = 512, WN = 4, MBW = 2, NBW = 2;
+constexpr int RB = 128;  // bytes per LDS row: 128 fp8 channels
+constexpr int S = 3;     // ring stages
+constexpr int A_BYTES = BM * RB, AS_BYTES = BM * 4, B_BYTES = BN * RB;
+constexpr int AS_BASE = S * A_BYTES;
+constexpr int B_BASE = AS_BASE + S * AS_BYTES;
+constexpr int RED_BASE = B_BASE + S * B_BYTES;  // gate/up epilogue: row maxima per column wave
+constexpr int LDS_BYTES = RED_BASE + BM * WN * 4;
+constexpr int A_INST = 2, B_INST = 4;            // 16-byte-per-lane DMAs per wave and K tile
+constexpr int INST = A_INST + 1 + B_INST;        // + one 4-byte-per-lane DMA of row scales
+}  // namespace w8
+
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+// One wave-wide 4-byte-per-lane DMA (row scales): lane l's 4 bytes at
+// base + voff(l) land at LDS byte address lds + 4*l.
+__device__ __forceinline__ void dma4(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :: "v"(voff), "s"(wave_uniform(base)), "s"(lds) : "memory");
+}
+
+template <int KIND>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void grouped_gemm_w8a8_kernel(GemmParams p) {
+  using namespace w8;
+  constexpr bool GATEUP = KIND == kGateUp;
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+  static_assert(AS_BASE >= (2 * kMaxExperts + 2 + NT / kWave) * 4, "scheduler tables");
+  __shared__ __attribute__((aligned(1024))) char smem_raw[LDS_BYTES];
+
+  Tile t;
+  {
+    int* s_tp = reinterpret_cast<int*>(smem_raw);
+    int* s_exp = s_tp + kMaxExperts + 1;
+    int* s_wave = s_exp + kMaxExperts + 1;
+    if (!locate_tile<BM, BN, NT>(p, s_tp, s_exp, s_wave, t)) return;
+    __syncthreads();  // every lane has its tile before the DMA overwrites the tables
+  }
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem_raw);
+  const int nk = p.K / 128;  // K tiles = scale blocks along K
+
+  // DMA: instruction q of this wave moves rows (wave + 8q)*8 .. +8 of the A
+  // or B stage; lane l writes 16 bytes at (row l/8, physical chunk l%8), so it
+  // fetches logical chunk (l%8) ^ swizzle(row).  The row-scale DMA of wave w
+  // covers rows (w%2)*64 .. +64 (four waves write each half, the same bytes).
+  const char* abase = reinterpret_cast<const char*>(p.a8);
+  const char* asbase = reinterpret_cast<const char*>(p.a_scale);
+  const char* bbase = reinterpret_cast<const char*>(group_weights(p, t.e, 1));
+  auto src_row = [&](int row) {
+    const int r = t.r0 + (row < t.rows_valid ? row : 0);
+    return GATEUP ? min(max(p.perm[r], 0), p.R - 1) / p.k : r;
+  };
+  uint32_t aoff[A_INST], boff[B_INST];
+  {
+    const int drow = lane >> 3, dpc = lane & 7;
+#pragma unroll
+    for (int q = 0; q < A_INST; ++q) {
+      const int row = (wave + 8 * q) * 8 + drow;
+      aoff[q] = (uint32_t)src_row(row) * (uint32_t)p.K + (uint32_t)((dpc ^ swz<RB>(row)) * 16);
+    }
+#pragma unroll
+    for (int q = 0; q < B_INST; ++q) {
+      const int j = (wave + 8 * q) * 8 + drow;
+      boff[q] = (uint32_t)weight_row<GATEUP, BN>(p, t.tn, j) * (uint32_t)p.K +
+                (uint32_t)((dpc ^ swz<RB>(j)) * 16);
+    }
+  }
+  const uint32_t asoff = (uint32_t)src_row((wave & 1) * 64 + lane) * (uint32_t)nk * 4u;
+  // K tile kt (its A rows, their scales, its B rows) into stage kt % S
+  auto issue = [&](int kt) {
+    const int st = kt % S;
+#pragma unroll
+    for (int q = 0; q < A_INST; ++q)
+      dma16(abase + kt * RB, aoff[q], lds0 + st * A_BYTES + (wave + 8 * q) * 8 * RB);
+    dma4(asbase + kt * 4, asoff, lds0 + AS_BASE + st * AS_BYTES + (wave & 1) * 256);
+#pragma unroll
+    for (int q = 0; q < B_INST; ++q)
+      dma16(bbase + kt * RB, boff[q], lds0 + B_BASE + st * B_BYTES + (wave + 8 * q) * 8 * RB);
+  };
+
+  const int wm = wave / WN, wn = wave % WN;
+  const int lrow = lane & 31;
+  const int khalf = lane >> 5;
+  const int am0 = wm * MBW * 32;
+  const int a_lane_off = (am0 + lrow) * RB;
+  int b_lane_off[NBW];
+  const CONST_AS float* sc[NBW];  // per N block: its row of weight block scales
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) {
+    const int br = block_row<GATEUP, BN, NBW>(wn, j);
+    b_lane_off[j] = (br + lrow) * RB;
+    sc[j] = (const CONST_AS float*)wave_uniform(
+        group_scales(p, t.e) + (size_t)(weight_row<GATEUP, BN>(p, t.tn, br) / 128) * nk);
+  }
+  const int s_l = swz<RB>(lrow);  // rows am0 + 32i + lrow share lrow's swizzle
+  const int mb_live =
+      __builtin_amdgcn_readfirstlane(max(0, min(MBW, ceil_div(t.rows_valid - am0, 32))));
+  const LDS_AS char* smem = (const LDS_AS char*)smem_raw;
+
+  // the 32 bytes of K step kk (0, 1) of the row at lane_off, for this lane
+  auto frag = [&](const LDS_AS char* base, int lane_off, int kk) {
+    const int c0 = kk * 4 + khalf * 2;
+    const u32x4 lo = *reinterpret_cast<const LDS_AS u32x4*>(base + lane_off + ((c0 ^ s_l) << 4));
+    const u32x4 hi =
+        *reinterpret_cast<const LDS_AS u32x4*>(base + lane_off + (((c0 + 1) ^ s_l) << 4));
+    return i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+                 (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+  };
+  i32x8 fa[2][MBW], fb[2][NBW];
+  auto load_frags = [&](int st, int kk) {
+    const LDS_AS char* as = smem + st * A_BYTES;
+    const LDS_AS char* bs = smem + B_BASE + st * B_BYTES;
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) fb[kk][j] = frag(bs, b_lane_off[j], kk);
+#pragma unroll
+    for (int i = 0; i < MBW; ++i) fa[kk][i] = frag(as, a_lane_off + i * 32 * RB, kk);
+  };
+  auto mma = [&](const i32x8& b, const i32x8& a, const f32x16& c) {
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b, a, c, 0, 0, 0, 127, 0, 127);
+  };
+
+  f32x16 acc[MBW][NBW], part[MBW][NBW];
+#pragma unroll
+  for (int i = 0; i < MBW; ++i)
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) acc[i][j] = f32x16{};
+
+  // prologue: K tiles 0 and 1 in flight, tile 0 landed
+  issue(0);
+  if (nk > 1) {
+    issue(1);
+    wait_vmcnt<INST>();
+  } else {
+    wait_vmcnt<0>();
+  }
+  lds_barrier();
+  load_frags(0, 0);
+  int st = 0;  // stage of tile kt
+  for (int kt = 0; kt < nk; ++kt) {
+    // this tile's scales: weight blocks (scalar loads) and rows (LDS); both
+    // are read before the tile's barrier, after which the stage is refilled
+    float wsc[NBW], rsc[MBW];
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) wsc[j] = sc[j][kt];
+#pragma unroll
+    for (int i = 0; i < MBW; ++i)
+      rsc[i] = *reinterpret_cast<const LDS_AS float*>(smem + AS_BASE + st * AS_BYTES +
+                                                      (am0 + i * 32 + lrow) * 4);
+    // k-step 0: DMA of tile kt+2 into the stage tile kt-1 released, the
+    // fragments of k-step 1, the MFMAs of k-step 0 (from zero)
+    if (kt + 2 < nk) issue(kt + 2);
+    load_frags(st, 1);
+#pragma unroll
+    for (int i = 0; i < MBW; ++i)
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) part[i][j] = mma(fb[0][j], fa[0][i], f32x16{});
+    // k-step 1: half the MFMAs, the tile boundary, the other half
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) part[0][j] = mma(fb[1][j], fa[1][0], part[0][j]);
+    const int st_next = st + 1 == S ? 0 : st + 1;
+    if (kt + 1 < nk) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      if (kt + 2 < nk) wait_vmcnt<INST>();
+      else wait_vmcnt<0>();
+      lds_barrier();
+      load_frags(st_next, 0);
+    }
+#pragma unroll
+    for (int i = 1; i < MBW; ++i)
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) part[i][j] = mma(fb[1][j], fa[1][i], part[i][j]);
+    // promotion of the tile's partial sums
+#pragma unroll
+    for (int i = 0; i < MBW; ++i)
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) {
+        const float f = rsc[i] * wsc[j];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] += f * part[i][j][v];
+      }
+    st = st_next;
+  }
+
+  if constexpr (GATEUP) {
+    // h = bf16(silu(g) * u), then per row over the tile's 128 h columns:
+    // s = amax / 448, q = e4m3(h / s).  This wave holds 32 of the columns
+    // (gate block j = 0 paired with up block j = 1), half in each lane half.
+    float* red = reinterpret_cast<float*>(smem_raw + RED_BASE);  // [BM][WN]
+    float hv[MBW][16];
+#pragma unroll
+    for (int i = 0; i < MBW; ++i) {
+      float m = 0.0f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float h = silu_mul(acc[i][0][v], acc[i][1][v]);
+        hv[i][v] = __uint_as_float(f32_to_bf16_bits(h) << 16);
+        m = fmaxf(m, fabsf(hv[i][v]));
+      }
+      m = fmaxf(m, __shfl_xor(m, 32));
+      if (khalf == 0) red[(am0 + i * 32 + lrow) * WN + wn] = m;
+    }
+    __syncthreads();
+    const int nkh = p.I / 128;  // h scale blocks per row
+#pragma unroll
+    for (int i = 0; i < MBW; ++i) {
+      const int rr = am0 + i * 32 + lrow;
+      if (rr >= t.rows_valid) continue;
+      const int r = t.r0 + rr;
+      float m = 0.0f;
+#pragma unroll
+      for (int w = 0; w < WN; ++w) m = fmaxf(m, red[rr * WN + w]);
+      const float s = m > 0.0f ? m / 448.0f : 1.0f;
+      uint8_t* qrow = p.hq + (size_t)r * p.I + t.tn * (BN / 2) + wn * 32;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int c = 8 * g + 4 * khalf;
+        *reinterpret_cast<uint32_t*>(qrow + c) =
+            pack_e4m3x4(hv[i][4 * g] / s, hv[i][4 * g + 1] / s, hv[i][4 * g + 2] / s,
+                        hv[i][4 * g + 3] / s);
+      }
+      if (wn == 0 && khalf == 0) p.hs[(size_t)r * nkh + t.tn] = s;
+    }
+  } else {
+    const RowInfo<MBW> ri = row_info<KIND, MBW>(p, t, am0, mb_live);
+    epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, ri, acc);
+  }
+}
+
+template <int KIND>
+hipError_t launch_w8a8(const GemmParams& p, int R, int E, hipStream_t stream) {
+  const long long grid = grid_tiles(R, E, w8::BM, w8::BN, p.N);
+  if (grid <= 0) return hipSuccess;
+  if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((grouped_gemm_w8a8_kernel<KIND>), dim3((unsigned)grid), dim3(w8::NT), 0,
+                     stream, p);
+  return hipGetLastError();
+}
+
 // Tile shapes (N a multiple of 256 takes the LDS-DMA kernels):
 //   bf16, prefill-sized: 256x256 tiles, 8 waves of 128x64 in ping-pong, BK=64;
 //   fp8 weights: 96x512 tiles (a decode batch's ~50-90 rows per expert fit
@@ -1185,6 +1450,13 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
   g.K = a.H;
   g.h = a.h;
   const int R = a.T * a.k;
+  if (a.act8) {
+    g.a8 = a.xq;
+    g.a_scale = a.xs;
+    g.hq = a.hq;
+    g.hs = a.hs;
+    return launch_w8a8<kGateUp>(g, R, a.E, stream);
+  }
   return a.fp8 ? launch_kind<kGateUp, true>(g, R, a.E, small_rows(a), stream)
                : launch_kind<kGateUp, false>(g, R, a.E, small_rows(a), stream);
 }
@@ -1201,6 +1473,12 @@ hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
   g.y = a.y;
   g.down = true;
   const int R = a.T * a.k;
+  if (a.act8) {
+    g.a8 = a.hq;
+    g.a_scale = a.hs;
+    return a.epilogue == kDownWeighted ? launch_w8a8<kDownWeightedK>(g, R, a.E, stream)
+                                       : launch_w8a8<kDownPlainK>(g, R, a.E, stream);
+  }
   const bool sm = small_rows(a);
   if (a.epilogue == kDownWeighted)
     return a.fp8 ? launch_kind<kDownWeightedK, true>(g, R, a.E, sm, stream)

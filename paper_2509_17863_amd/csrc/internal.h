@@ -47,7 +47,20 @@ struct FfnArgs {
   // come from the per-layer records (w_* and s_* above are then unused)
   const eaas_layer_weights* layers = nullptr;
   int e_layer = 0;
+  // fp8 activations (with fp8 weights): x and h quantized per row and 128
+  // channels; h is then held only as hq / hs
+  bool act8 = false;
+  const uint8_t* xq = nullptr;  // [T,H]
+  const float* xs = nullptr;    // [T,H/128]
+  uint8_t* hq = nullptr;        // [R,I]
+  float* hs = nullptr;          // [R,I/128]
 };
+
+// x [rows,K] bf16 -> q [rows,K] e4m3fn and s [rows,K/128]: per row and 128
+// channels, s = amax/448 (1 if all zero), q = e4m3(x/s) (nearest even,
+// saturating).
+hipError_t launch_quantize_rows(const uint16_t* x, long long rows, int K, uint8_t* q, float* s,
+                                hipStream_t stream);
 
 // Gate/up GEMM with the SiLU*mul epilogue into h.
 hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream);

@@ -12,7 +12,7 @@ from pathlib import Path
 import torch
 
 __all__ = [
-    "EAAS_OK", "EAAS_BF16", "EAAS_FP8_E4M3", "EAAS_FP32", "EaasError", "lib",
+    "EAAS_OK", "EAAS_BF16", "EAAS_FP8_E4M3", "EAAS_FP32", "EAAS_FP8_E4M3_A8", "EaasError", "lib",
     "library_path", "eaas_workspace_bytes", "eaas_route_permute",
     "eaas_expert_ffn_grouped", "eaas_unpermute_combine", "eaas_expert_forward",
     "eaas_status_string", "eaas_expert_forward_profiled", "alloc_routing",
@@ -20,16 +20,19 @@ __all__ = [
     "alloc_segments_workspace", "segment_table", "eaas_expert_forward_segments",
     "EAAS_SLOT_EMPTY", "EAAS_SLOT_READY", "EAAS_SLOT_DONE", "EAAS_SLOT_OFFLINE",
     "eaas_server_workspace_bytes", "alloc_server_workspace", "slot_table", "layer_table",
-    "eaas_server_step",
+    "eaas_server_step", "eaas_quantize_rows_fp8", "eaas_workspace_region", "workspace_view",
+    "EAAS_WS_H", "EAAS_WS_HQ", "EAAS_WS_HS", "EAAS_WS_XQ", "EAAS_WS_XS", "EAAS_WS_STAGE",
 ]
 
 EAAS_OK = 0
-EAAS_BF16, EAAS_FP8_E4M3, EAAS_FP32 = 0, 1, 2
+EAAS_BF16, EAAS_FP8_E4M3, EAAS_FP32, EAAS_FP8_E4M3_A8 = 0, 1, 2, 3
 EAAS_SLOT_EMPTY, EAAS_SLOT_READY, EAAS_SLOT_DONE, EAAS_SLOT_OFFLINE = 0, 1, 2, 3
+EAAS_WS_H, EAAS_WS_HQ, EAAS_WS_HS, EAAS_WS_XQ, EAAS_WS_XS, EAAS_WS_STAGE = range(6)
 EXPORTED = ("eaas_workspace_bytes", "eaas_route_permute", "eaas_expert_ffn_grouped",
             "eaas_unpermute_combine", "eaas_expert_forward", "eaas_expert_forward_profiled",
             "eaas_status_string", "eaas_segments_workspace_bytes",
-            "eaas_expert_forward_segments", "eaas_server_workspace_bytes", "eaas_server_step")
+            "eaas_expert_forward_segments", "eaas_server_workspace_bytes", "eaas_server_step",
+            "eaas_quantize_rows_fp8", "eaas_workspace_region")
 
 _LIB_PATH = Path(__file__).resolve().parent / "libeaas.so"
 _lib = None
@@ -87,6 +90,10 @@ def lib() -> ctypes.CDLL:
         L.eaas_server_workspace_bytes.restype = sz
         L.eaas_server_step.argtypes = [sp, vp, i32, vp, i32, i32, vp, sz, vp]
         L.eaas_server_step.restype = i32
+        L.eaas_quantize_rows_fp8.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, vp, vp, vp]
+        L.eaas_quantize_rows_fp8.restype = i32
+        L.eaas_workspace_region.argtypes = [sp, i32, i32, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+        L.eaas_workspace_region.restype = i32
         L.eaas_status_string.argtypes = [i32]
         L.eaas_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -130,12 +137,36 @@ def _check(status: int, where: str) -> None:
         raise EaasError(status, where)
 
 
-def _wdtype(w: torch.Tensor) -> int:
+def _wdtype(w: torch.Tensor, act8: bool = False) -> int:
     if w.element_size() == 1:
-        return EAAS_FP8_E4M3
+        return EAAS_FP8_E4M3_A8 if act8 else EAAS_FP8_E4M3
+    if act8:
+        raise ValueError("fp8 activations need fp8-e4m3 (1-byte) weights")
     if w.element_size() == 2:
         return EAAS_BF16
     raise ValueError("weights must be bf16 (2-byte) or fp8-e4m3 (1-byte) tensors")
+
+
+def eaas_workspace_region(T, H, I, E, k, w_dtype, region) -> tuple[int, int]:
+    """(byte offset, bytes) of an intermediate inside the workspace."""
+    s = _shape(T, H, I, E, k)
+    off, n = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().eaas_workspace_region(ctypes.byref(s), int(w_dtype), int(region),
+                                       ctypes.byref(off), ctypes.byref(n)), "eaas_workspace_region")
+    return off.value, n.value
+
+
+def workspace_view(ws: torch.Tensor, T, H, I, E, k, w_dtype, region) -> torch.Tensor:
+    """The bytes of one workspace region, as a uint8 view of `ws`."""
+    off, n = eaas_workspace_region(T, H, I, E, k, w_dtype, region)
+    return ws[off: off + n]
+
+
+def eaas_quantize_rows_fp8(x: torch.Tensor, q: torch.Tensor, s: torch.Tensor, stream=None) -> None:
+    """x [rows, K] bf16 -> q [rows, K] e4m3fn codes (uint8), s [rows, K/128] fp32."""
+    rows, K = x.shape
+    _check(lib().eaas_quantize_rows_fp8(_p(x), rows, K, _p(q), _p(s), _stream(stream)),
+           "eaas_quantize_rows_fp8")
 
 
 def eaas_workspace_bytes(T, H, I, E, k, w_dtype=EAAS_BF16) -> int:
@@ -168,14 +199,15 @@ def eaas_route_permute(topk_ids: torch.Tensor, E: int, routing: dict, ws: torch.
 
 def eaas_expert_ffn_grouped(x: torch.Tensor, routing: dict, w_gate_up: torch.Tensor,
                             w_down: torch.Tensor, y_perm: torch.Tensor, ws: torch.Tensor,
-                            k: int, w_gate_up_scale=None, w_down_scale=None, stream=None) -> None:
+                            k: int, w_gate_up_scale=None, w_down_scale=None, stream=None,
+                            act8: bool = False) -> None:
     T, H = x.shape
     E, twoI, _ = w_gate_up.shape
     s = _shape(T, H, twoI // 2, E, k)
     r = _routing(routing)
     st = lib().eaas_expert_ffn_grouped(
         ctypes.byref(s), _p(x), ctypes.byref(r), _p(w_gate_up), _p(w_gate_up_scale),
-        _p(w_down), _p(w_down_scale), _wdtype(w_gate_up), _p(y_perm), _p(ws), ws.numel(),
+        _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8), _p(y_perm), _p(ws), ws.numel(),
         _stream(stream))
     _check(st, "eaas_expert_ffn_grouped")
 
@@ -195,9 +227,11 @@ def eaas_unpermute_combine(y_perm: torch.Tensor, routing: dict, topk_weights: to
 def eaas_expert_forward(x: torch.Tensor, topk_ids: torch.Tensor, topk_weights: torch.Tensor,
                         w_gate_up: torch.Tensor, w_down: torch.Tensor, out: torch.Tensor,
                         ws: torch.Tensor, w_gate_up_scale=None, w_down_scale=None,
-                        routing: dict | None = None, stream=None, events=None) -> None:
+                        routing: dict | None = None, stream=None, events=None,
+                        act8: bool = False) -> None:
     """events: optional 5 torch.cuda.Event(enable_timing=True) recorded on the
-    stream around routing, gate/up, down and combine (profiled entry point)."""
+    stream around routing, gate/up, down and combine (profiled entry point).
+    act8: fp8 activations with the fp8 weights (EAAS_FP8_E4M3_A8)."""
     T, H = x.shape
     E, twoI, _ = w_gate_up.shape
     k = topk_ids.shape[1]
@@ -205,7 +239,7 @@ def eaas_expert_forward(x: torch.Tensor, topk_ids: torch.Tensor, topk_weights: t
     r = _routing(routing)
     odt = EAAS_FP32 if out.dtype == torch.float32 else EAAS_BF16
     args = (ctypes.byref(s), _p(x), _p(topk_ids), _p(topk_weights), _p(w_gate_up),
-            _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up), _p(out), odt,
+            _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8), _p(out), odt,
             ctypes.byref(r) if r is not None else None, _p(ws), ws.numel(), _stream(stream))
     if events is None:
         _check(lib().eaas_expert_forward(*args), "eaas_expert_forward")

@@ -48,6 +48,7 @@ class Workload:
     seed: int
     zipf: float | None = None     # alpha of the per-expert logit bias, None = no bias
     wdtype: str = "bf16"          # "bf16" or "fp8"
+    act8: bool = False            # fp8 activations too (fp8 weights only)
 
     @property
     def R(self) -> int:
@@ -64,6 +65,9 @@ WORKLOADS = {
     "qwen3": Workload("qwen3", 8192, 2048, 768, 128, 8, 2, zipf=1.1),
     "dsv3_prefill": Workload("dsv3_prefill", 16384, 7168, 2048, 32, 8, 3, zipf=1.2),
     "dsv3_decode": Workload("dsv3_decode", 256, 7168, 2048, 32, 8, 4, wdtype="fp8"),
+    # dsv3_prefill's batch and routing with fp8 weights and fp8 activations
+    "dsv3_prefill_w8a8": Workload("dsv3_prefill_w8a8", 16384, 7168, 2048, 32, 8, 3, zipf=1.2,
+                                  wdtype="fp8", act8=True),
 }
 
 
@@ -158,6 +162,7 @@ def make_workload(name: str, weights: bool = True) -> dict:
     wl = WORKLOADS[name]
     d = make_inputs(wl.T, wl.H, wl.I, wl.E, wl.k, wl.seed, wl.zipf, wl.wdtype, weights)
     d["workload"] = asdict(wl)
+    d["act8"] = wl.act8
     return d
 
 

@@ -13,7 +13,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def _declared():
     src = open(os.path.join(ROOT, "include", "eaas.h")).read()
-    return sorted(set(re.findall(r"\b(eaas_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(eaas_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_header_declares_the_exported_set():
@@ -185,3 +185,39 @@ def test_server_workspace_and_validation():
     assert call(w=None) == -3
     assert call(wb=128) == -3
     assert call(n=0, slots=None, layers=None) == 0
+
+
+def test_fp8_activation_mode_host_validation():
+    L = eaas.lib()
+    A8 = eaas.EAAS_FP8_E4M3_A8
+    # H must be a multiple of 256 (the down projection's 256-wide N tiles)
+    assert eaas.eaas_workspace_bytes(64, 384, 128, 8, 2, A8) == 0
+    n8 = eaas.eaas_workspace_bytes(64, 512, 128, 8, 2, eaas.EAAS_FP8_E4M3)
+    na8 = eaas.eaas_workspace_bytes(64, 512, 128, 8, 2, A8)
+    assert na8 >= n8 + 64 * 512 + 64 * 4 * 4  # + quantized x and its scales
+    s = shape(H=512)
+    big = 1 << 34
+
+    def fwd(wdt=A8, sgu=FAKE, sd=FAKE, sh=s):
+        return L.eaas_expert_forward(ctypes.byref(sh), FAKE, FAKE, FAKE, FAKE, sgu, FAKE, sd, wdt,
+                                     FAKE * 64, 0, None, FAKE, big, None)
+
+    assert fwd(sgu=None) == -1            # fp8 weights need their scales
+    assert fwd(sh=shape(H=384)) == -2     # H not a multiple of 256
+    # the batched entry points do not take fp8 activations
+    assert L.eaas_segments_workspace_bytes(ctypes.byref(s), A8) == 0
+    assert L.eaas_server_workspace_bytes(ctypes.byref(s), 1, A8) == 0
+    assert L.eaas_expert_forward_segments(ctypes.byref(s), FAKE, FAKE, 1, FAKE, FAKE, FAKE, FAKE,
+                                          A8, 0, FAKE, big, None) == -2
+
+
+def test_quantize_rows_rejects_bad_args():
+    L = eaas.lib()
+    assert L.eaas_quantize_rows_fp8(FAKE, -1, 128, FAKE, FAKE, None) == -1
+    assert L.eaas_quantize_rows_fp8(FAKE, 4, 0, FAKE, FAKE, None) == -1
+    assert L.eaas_quantize_rows_fp8(FAKE, 4, 100, FAKE, FAKE, None) == -2
+    assert L.eaas_quantize_rows_fp8(FAKE, 1 << 24, 1 << 10, FAKE, FAKE, None) == -2
+    assert L.eaas_quantize_rows_fp8(None, 4, 128, FAKE, FAKE, None) == -1
+    assert L.eaas_quantize_rows_fp8(FAKE + 8, 4, 128, FAKE, FAKE, None) == -1
+    assert L.eaas_quantize_rows_fp8(FAKE, 4, 128, None, FAKE, None) == -1
+    assert L.eaas_quantize_rows_fp8(None, 0, 128, None, None, None) == 0
