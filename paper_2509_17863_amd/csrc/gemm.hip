@@ -1142,23 +1142,37 @@ hipError_t launch_pp(const GemmParams& p, int R, int E, hipStream_t stream) {
 // the bf16 loops (same DMA geometry and swizzle).  The block-scaled MFMA
 // (v_mfma_scale_f32_32x32x64_f8f6f4, unit block scales) takes 32 bytes of K
 // per lane; A and B fragments hold the same K bytes in the same order, so the
-// two MFMAs of a 32x32 block per K tile give that tile's fp32 dot products
-// in `part`, and then acc += (row scale * weight block scale) * part.
-// 8 waves of 64x64 (2x2 blocks of 32x32) over a 128x256 tile; a 3-stage
-// ring holds each K tile's token rows, their row scales and the weight rows.
-// The gate/up epilogue quantizes h per row over the tile's 128 h columns (the
-// 4 column waves combine their row maxima in LDS).
+// two MFMAs of a 32x32 block per K tile give that tile's dot products in
+// `part`, and acc += (row scale * weight block scale) * part.  (The MFMA's
+// internal sums are narrower than fp32; promoting every 128 channels keeps
+// their error to one K tile's worth.)
+//
+// Tile 128x256, 8 waves of 64x64 in two groups of four (group g: rows
+// 64g..64g+63, all 256 columns).  As in the bf16 ping-pong kernel, the groups
+// alternate, phase by phase, between M (fragment reads of a K tile and the
+// DMA share of the group) and C (the tile's 8 MFMAs, with the promotion of
+// the previous tile's partial sums beside them), so each SIMD's matrix pipe
+// is fed by one of its two waves while the other reads:
+//   group 0, phase 2t:   M(t): DMA of A tile t+1 (t >= 1, with its row
+//                        scales), fragments and scales of tile t
+//   group 0, phase 2t+1: C(t), then wait until A tile t+1 has landed
+//   group 1, phase 2t+1: M(t): DMA of B tile t+2, fragments and scales of
+//                        tile t, wait until B tile t+1 has landed
+//   group 1, phase 2t+2: C(t)
+// A has 2 LDS stages and B 3; a stage is refilled only after both groups have
+// read it.  The gate/up epilogue quantizes h per row over the tile's 128 h
+// columns (the 4 waves of a group combine their row maxima in LDS).
 namespace w8 {
 constexpr int BM = 128, BN = 256, NT = 512, WN = 4, MBW = 2, NBW = 2;
 constexpr int RB = 128;  // bytes per LDS row: 128 fp8 channels
-constexpr int S = 3;     // ring stages
+constexpr int SA = 2, SB = 3;
 constexpr int A_BYTES = BM * RB, AS_BYTES = BM * 4, B_BYTES = BN * RB;
-constexpr int AS_BASE = S * A_BYTES;
-constexpr int B_BASE = AS_BASE + S * AS_BYTES;
-constexpr int RED_BASE = B_BASE + S * B_BYTES;  // gate/up epilogue: row maxima per column wave
+constexpr int AS_BASE = SA * A_BYTES;
+constexpr int B_BASE = AS_BASE + SA * AS_BYTES;
+constexpr int RED_BASE = B_BASE + SB * B_BYTES;  // gate/up epilogue: row maxima per column wave
 constexpr int LDS_BYTES = RED_BASE + BM * WN * 4;
-constexpr int A_INST = 2, B_INST = 4;            // 16-byte-per-lane DMAs per wave and K tile
-constexpr int INST = A_INST + 1 + B_INST;        // + one 4-byte-per-lane DMA of row scales
+constexpr int A_INST = 4;  // 16-byte-per-lane DMAs of a group-0 wave per K tile (+1 of scales)
+constexpr int B_INST = 8;  // of a group-1 wave
 }  // namespace w8
 
 typedef int i32x8 __attribute__((ext_vector_type(8)));
@@ -1190,52 +1204,61 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  const int grp = wave >> 2;  // 0: rows 0-63, streams A; 1: rows 64-127, streams B
+  const int wn = wave & 3;
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem_raw);
   const int nk = p.K / 128;  // K tiles = scale blocks along K
 
-  // DMA: instruction q of this wave moves rows (wave + 8q)*8 .. +8 of the A
-  // or B stage; lane l writes 16 bytes at (row l/8, physical chunk l%8), so it
-  // fetches logical chunk (l%8) ^ swizzle(row).  The row-scale DMA of wave w
-  // covers rows (w%2)*64 .. +64 (four waves write each half, the same bytes).
-  const char* abase = reinterpret_cast<const char*>(p.a8);
-  const char* asbase = reinterpret_cast<const char*>(p.a_scale);
-  const char* bbase = reinterpret_cast<const char*>(group_weights(p, t.e, 1));
+  // DMA: instruction q of wave wn of a group moves rows (wn + 4q)*8 .. +8 of
+  // the group's operand; lane l writes 16 bytes at (row l/8, physical chunk
+  // l%8), so it fetches logical chunk (l%8) ^ swizzle(row).  Group 0's scale
+  // DMA from wave wn covers rows (wn%2)*64 .. +64 (two waves write each half,
+  // the same bytes).
   auto src_row = [&](int row) {
     const int r = t.r0 + (row < t.rows_valid ? row : 0);
     return GATEUP ? min(max(p.perm[r], 0), p.R - 1) / p.k : r;
   };
-  uint32_t aoff[A_INST], boff[B_INST];
+  const char* dbase;
+  uint32_t doff[B_INST];
+  uint32_t asoff = 0;
   {
     const int drow = lane >> 3, dpc = lane & 7;
+    if (grp == 0) {
+      dbase = reinterpret_cast<const char*>(p.a8);
 #pragma unroll
-    for (int q = 0; q < A_INST; ++q) {
-      const int row = (wave + 8 * q) * 8 + drow;
-      aoff[q] = (uint32_t)src_row(row) * (uint32_t)p.K + (uint32_t)((dpc ^ swz<RB>(row)) * 16);
-    }
+      for (int q = 0; q < B_INST; ++q) {
+        const int row = (wn + 4 * (q % A_INST)) * 8 + drow;
+        doff[q] = (uint32_t)src_row(row) * (uint32_t)p.K + (uint32_t)((dpc ^ swz<RB>(row)) * 16);
+      }
+      asoff = (uint32_t)src_row((wn & 1) * 64 + lane) * (uint32_t)nk * 4u;
+    } else {
+      dbase = reinterpret_cast<const char*>(group_weights(p, t.e, 1));
 #pragma unroll
-    for (int q = 0; q < B_INST; ++q) {
-      const int j = (wave + 8 * q) * 8 + drow;
-      boff[q] = (uint32_t)weight_row<GATEUP, BN>(p, t.tn, j) * (uint32_t)p.K +
-                (uint32_t)((dpc ^ swz<RB>(j)) * 16);
+      for (int q = 0; q < B_INST; ++q) {
+        const int j = (wn + 4 * q) * 8 + drow;
+        doff[q] = (uint32_t)weight_row<GATEUP, BN>(p, t.tn, j) * (uint32_t)p.K +
+                  (uint32_t)((dpc ^ swz<RB>(j)) * 16);
+      }
     }
   }
-  const uint32_t asoff = (uint32_t)src_row((wave & 1) * 64 + lane) * (uint32_t)nk * 4u;
-  // K tile kt (its A rows, their scales, its B rows) into stage kt % S
+  const char* asbase = reinterpret_cast<const char*>(p.a_scale);
+  // DMA of K tile kt of this group's operand into its ring slot
   auto issue = [&](int kt) {
-    const int st = kt % S;
+    if (grp == 0) {
+      const uint32_t dst = lds0 + (kt % SA) * A_BYTES + wn * 8 * RB;
 #pragma unroll
-    for (int q = 0; q < A_INST; ++q)
-      dma16(abase + kt * RB, aoff[q], lds0 + st * A_BYTES + (wave + 8 * q) * 8 * RB);
-    dma4(asbase + kt * 4, asoff, lds0 + AS_BASE + st * AS_BYTES + (wave & 1) * 256);
+      for (int q = 0; q < A_INST; ++q) dma16(dbase + kt * RB, doff[q], dst + q * 4 * 8 * RB);
+      dma4(asbase + kt * 4, asoff, lds0 + AS_BASE + (kt % SA) * AS_BYTES + (wn & 1) * 256);
+    } else {
+      const uint32_t dst = lds0 + B_BASE + (kt % SB) * B_BYTES + wn * 8 * RB;
 #pragma unroll
-    for (int q = 0; q < B_INST; ++q)
-      dma16(bbase + kt * RB, boff[q], lds0 + B_BASE + st * B_BYTES + (wave + 8 * q) * 8 * RB);
+      for (int q = 0; q < B_INST; ++q) dma16(dbase + kt * RB, doff[q], dst + q * 4 * 8 * RB);
+    }
   };
 
-  const int wm = wave / WN, wn = wave % WN;
   const int lrow = lane & 31;
   const int khalf = lane >> 5;
-  const int am0 = wm * MBW * 32;
+  const int am0 = grp * MBW * 32;
   const int a_lane_off = (am0 + lrow) * RB;
   int b_lane_off[NBW];
   const CONST_AS float* sc[NBW];  // per N block: its row of weight block scales
@@ -1260,15 +1283,6 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
     return i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
                  (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
   };
-  i32x8 fa[2][MBW], fb[2][NBW];
-  auto load_frags = [&](int st, int kk) {
-    const LDS_AS char* as = smem + st * A_BYTES;
-    const LDS_AS char* bs = smem + B_BASE + st * B_BYTES;
-#pragma unroll
-    for (int j = 0; j < NBW; ++j) fb[kk][j] = frag(bs, b_lane_off[j], kk);
-#pragma unroll
-    for (int i = 0; i < MBW; ++i) fa[kk][i] = frag(as, a_lane_off + i * 32 * RB, kk);
-  };
   auto mma = [&](const i32x8& b, const i32x8& a, const f32x16& c) {
     return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b, a, c, 0, 0, 0, 127, 0, 127);
   };
@@ -1277,63 +1291,113 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
 #pragma unroll
   for (int i = 0; i < MBW; ++i)
 #pragma unroll
-    for (int j = 0; j < NBW; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < NBW; ++j) {
+      acc[i][j] = f32x16{};
+      part[i][j] = f32x16{};
+    }
+  i32x8 fa[2][MBW], fb[2][NBW];
+  // scale products (row scale x weight block scale): f of the tile in
+  // `part` (0 before the first), fn of the tile whose fragments are loaded
+  float f[MBW][NBW], fn[MBW][NBW];
+#pragma unroll
+  for (int i = 0; i < MBW; ++i)
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) f[i][j] = fn[i][j] = 0.0f;
 
-  // prologue: K tiles 0 and 1 in flight, tile 0 landed
-  issue(0);
-  if (nk > 1) {
-    issue(1);
-    wait_vmcnt<INST>();
-  } else {
-    wait_vmcnt<0>();
-  }
-  lds_barrier();
-  load_frags(0, 0);
-  int st = 0;  // stage of tile kt
-  for (int kt = 0; kt < nk; ++kt) {
-    // this tile's scales: weight blocks (scalar loads) and rows (LDS); both
-    // are read before the tile's barrier, after which the stage is refilled
+  auto phase_end = [&]() {
+    // keep the scheduler from moving MFMAs or LDS reads across the barrier
+    __builtin_amdgcn_sched_barrier(0);
+    lds_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // M(kt): fragments and scales of tile kt; promotion of the previous tile
+  auto load_tile = [&](int kt) {
+    const LDS_AS char* as = smem + (kt % SA) * A_BYTES;
+    const LDS_AS char* bs = smem + B_BASE + (kt % SB) * B_BYTES;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) fb[kk][j] = frag(bs, b_lane_off[j], kk);
+#pragma unroll
+      for (int i = 0; i < MBW; ++i) fa[kk][i] = frag(as, a_lane_off + i * 32 * RB, kk);
+    }
     float wsc[NBW], rsc[MBW];
 #pragma unroll
     for (int j = 0; j < NBW; ++j) wsc[j] = sc[j][kt];
 #pragma unroll
     for (int i = 0; i < MBW; ++i)
-      rsc[i] = *reinterpret_cast<const LDS_AS float*>(smem + AS_BASE + st * AS_BYTES +
+      rsc[i] = *reinterpret_cast<const LDS_AS float*>(smem + AS_BASE + (kt % SA) * AS_BYTES +
                                                       (am0 + i * 32 + lrow) * 4);
-    // k-step 0: DMA of tile kt+2 into the stage tile kt-1 released, the
-    // fragments of k-step 1, the MFMAs of k-step 0 (from zero)
-    if (kt + 2 < nk) issue(kt + 2);
-    load_frags(st, 1);
 #pragma unroll
     for (int i = 0; i < MBW; ++i)
 #pragma unroll
-      for (int j = 0; j < NBW; ++j) part[i][j] = mma(fb[0][j], fa[0][i], f32x16{});
-    // k-step 1: half the MFMAs, the tile boundary, the other half
-#pragma unroll
-    for (int j = 0; j < NBW; ++j) part[0][j] = mma(fb[1][j], fa[1][0], part[0][j]);
-    const int st_next = st + 1 == S ? 0 : st + 1;
-    if (kt + 1 < nk) {
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      if (kt + 2 < nk) wait_vmcnt<INST>();
-      else wait_vmcnt<0>();
-      lds_barrier();
-      load_frags(st_next, 0);
-    }
-#pragma unroll
-    for (int i = 1; i < MBW; ++i)
-#pragma unroll
-      for (int j = 0; j < NBW; ++j) part[i][j] = mma(fb[1][j], fa[1][i], part[i][j]);
-    // promotion of the tile's partial sums
+      for (int j = 0; j < NBW; ++j) fn[i][j] = rsc[i] * wsc[j];
+    // the stage may be refilled right after the next barrier
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  };
+  // C(kt): the tile's MFMAs into `part`; before each block's first MFMA, the
+  // previous tile's partial sums of that block are promoted (VALU work that
+  // runs beside the matrix pipe)
+  auto mfmas = [&]() {
 #pragma unroll
     for (int i = 0; i < MBW; ++i)
 #pragma unroll
       for (int j = 0; j < NBW; ++j) {
-        const float f = rsc[i] * wsc[j];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) acc[i][j][v] += f * part[i][j][v];
+        for (int v = 0; v < 16; ++v) acc[i][j][v] += f[i][j] * part[i][j][v];
+        f[i][j] = fn[i][j];
+        part[i][j] = mma(fb[0][j], fa[0][i], f32x16{});
       }
-    st = st_next;
+#pragma unroll
+    for (int i = 0; i < MBW; ++i)
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) part[i][j] = mma(fb[1][j], fa[1][i], part[i][j]);
+  };
+
+  // prologue: each group's first two K tiles of its operand; tile 0 must
+  // have landed before the first barrier
+  constexpr int INST_G0 = A_INST + 1;
+  issue(0);
+  if (nk > 1) {
+    issue(1);
+    if (grp == 0) wait_vmcnt<INST_G0>();
+    else wait_vmcnt<B_INST>();
+  } else {
+    wait_vmcnt<0>();
   }
+  phase_end();
+  // both groups pass 2*nk + 1 phase barriers: group 1 idles in the first
+  // phase, group 0 in the last
+  if (grp == 0) {
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt >= 1 && kt + 1 < nk) issue(kt + 1);
+      load_tile(kt);
+      phase_end();
+      mfmas();
+      wait_vmcnt<0>();  // A tile kt+1 (issued in the previous phase) has landed
+      phase_end();
+    }
+    phase_end();
+  } else {
+    phase_end();
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + 2 < nk) issue(kt + 2);
+      load_tile(kt);
+      // B tile kt+1 has landed; B tile kt+2 may still be in flight
+      if (kt + 2 < nk) wait_vmcnt<B_INST>();
+      else wait_vmcnt<0>();
+      phase_end();
+      mfmas();
+      phase_end();
+    }
+  }
+  // promotion of the last tile
+#pragma unroll
+  for (int i = 0; i < MBW; ++i)
+#pragma unroll
+    for (int j = 0; j < NBW; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] += f[i][j] * part[i][j][v];
 
   if constexpr (GATEUP) {
     // h = bf16(silu(g) * u), then per row over the tile's 128 h columns:
