@@ -348,3 +348,38 @@ def test_fp8_mfma_accumulation_error(gpu, case):
         worst = max(worst, float(rel.max()))
     say(f"fp8 MFMA accumulation {case}: worst |dy| / sum|h w| = 2^{np.log2(worst):.1f}")
     assert worst <= MFMA_EPS
+
+
+def test_forward_w8a8_graph_replay_matches_eager(gpu):
+    """The fp8-activation step captured in a graph: every replay, with eager
+    work between replays, gives the eager result bit for bit."""
+    d = synth.make_inputs(200, 512, 256, 6, 2, 47, wdtype="fp8")
+    say("forward w8a8 graph replay")
+    dev = to_device(d)
+    E, twoI, _ = dev["w_gate_up"].shape
+    ws = eaas.alloc_workspace(200, 512, twoI // 2, E, 2, eaas.EAAS_FP8_E4M3_A8)
+    out = torch.zeros((200, 512), dtype=torch.float32, device="cuda")
+
+    def step():
+        eaas.eaas_expert_forward(dev["x"], dev["topk_ids"], dev["topk_weights"], dev["w_gate_up"],
+                                 dev["w_down"], out, ws, dev["w_gate_up_scale"],
+                                 dev["w_down_scale"], act8=True)
+
+    step()
+    torch.cuda.synchronize()
+    ref = out.clone()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for _ in range(3):
+        out.zero_()
+        ws.fill_(0x7F)  # the step must rebuild every intermediate itself
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int32), ref.view(torch.int32))
