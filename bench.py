@@ -223,7 +223,8 @@ def time_segments(d: dict, dev: dict, clients: int, steps: int, warmup: int, ms_
     def step():
         eaas.eaas_expert_forward_segments(table, counts, clients, T, k, dev["w_gate_up"],
                                           dev["w_down"], ws, eaas.EAAS_BF16,
-                                          dev["w_gate_up_scale"], dev["w_down_scale"])
+                                          dev["w_gate_up_scale"], dev["w_down_scale"],
+                                          act8=act8)
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()

@@ -84,8 +84,8 @@ enum eaas_dtype {
    * GEMMs on fp8 x fp8 MFMAs with fp32 accumulation, scaling each 128-wide K
    * block's partial sums by its row scale times its weight block scale (the
    * block-scaled fp8 GEMM of the grouped-GEMM engine named in §4.1).  Needs
-   * H a multiple of 256.  Accepted by eaas_workspace_bytes,
-   * eaas_expert_ffn_grouped, eaas_expert_forward(_profiled). */
+   * H a multiple of 256.  Accepted by every entry point that takes a
+   * weight dtype. */
   EAAS_FP8_E4M3_A8 = 3
 };
 

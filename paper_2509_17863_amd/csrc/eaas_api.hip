@@ -309,9 +309,8 @@ int eaas_expert_forward(const eaas_shape* s, const void* x, const int32_t* topk_
 }
 
 size_t eaas_segments_workspace_bytes(const eaas_shape* s, int w_dtype) {
-  if (check_shape(s) != EAAS_OK) return 0;
-  if (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3) return 0;
-  return layout(*s).seg_total;
+  if (eaas_workspace_bytes(s, w_dtype) == 0) return 0;
+  return layout(*s, w_dtype).seg_total;
 }
 
 int eaas_expert_forward_segments(const eaas_shape* s, const eaas_segment* segs,
@@ -321,13 +320,13 @@ int eaas_expert_forward_segments(const eaas_shape* s, const eaas_segment* segs,
                                  size_t ws_bytes, void* stream) {
   int st = check_shape(s);
   if (st != EAAS_OK) return st;
-  if (w_dtype == EAAS_FP8_E4M3_A8) return EAAS_ERR_UNSUPPORTED;  // single-batch entry points only
   if (n_seg < 0 || n_seg > kMaxSegments) return EAAS_ERR_INVALID_ARG;
+  if ((st = check_dtype_shape(s, w_dtype)) != EAAS_OK) return st;
   if (s->T == 0 || n_seg == 0) return EAAS_OK;
   if (!segs || !num_tokens || (out_dtype != EAAS_BF16 && out_dtype != EAAS_FP32) ||
       !weights_ok(w_gate_up, w_gate_up_scale, w_down, w_down_scale, w_dtype))
     return EAAS_ERR_INVALID_ARG;
-  const WsLayout L = layout(*s);
+  const WsLayout L = layout(*s, w_dtype);
   if (!ws || !aligned16(ws) || ws_bytes < L.seg_total) return EAAS_ERR_WORKSPACE;
   char* base = static_cast<char*>(ws);
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
@@ -353,12 +352,13 @@ int eaas_expert_forward_segments(const eaas_shape* s, const eaas_segment* segs,
   a.s_gate_up = w_gate_up_scale;
   a.w_down = w_down;
   a.s_down = w_down_scale;
-  a.fp8 = w_dtype == EAAS_FP8_E4M3;
+  set_dtype_args(a, w_dtype, base, L);
   a.h = reinterpret_cast<uint16_t*>(base + L.h);
   a.y = stage;
   a.topk_weights = w_cat;
   a.epilogue = kDownWeighted;
-  e = launch_gate_up(a, hs);
+  e = quantize_x(a, base, L, hs);
+  if (e == hipSuccess) e = launch_gate_up(a, hs);
   if (e == hipSuccess) e = launch_down(a, hs);
   if (e == hipSuccess)
     e = launch_seg_combine(segs, num_tokens, n_seg, cap, s->H, s->k, stage, rt.inv,
@@ -405,8 +405,8 @@ extern "C" {
 size_t eaas_server_workspace_bytes(const eaas_shape* s, int n_layers, int w_dtype) {
   eaas_shape g;
   if (server_shape(s, n_layers, &g) != EAAS_OK) return 0;
-  if (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3) return 0;
-  return slot_layout(layout(g).seg_total).total;
+  if (eaas_workspace_bytes(&g, w_dtype) == 0) return 0;
+  return slot_layout(layout(g, w_dtype).seg_total).total;
 }
 
 int eaas_server_step(const eaas_shape* s, const eaas_slot* slots, int n_slots,
@@ -415,12 +415,13 @@ int eaas_server_step(const eaas_shape* s, const eaas_slot* slots, int n_slots,
   eaas_shape g;
   int st = server_shape(s, n_layers, &g);
   if (st != EAAS_OK) return st;
-  if (w_dtype == EAAS_FP8_E4M3_A8) return EAAS_ERR_UNSUPPORTED;  // single-batch entry points only
   if (n_slots < 0 || n_slots > kMaxSegments) return EAAS_ERR_INVALID_ARG;
+  if ((st = check_dtype_shape(&g, w_dtype)) != EAAS_OK) return st;
   if (n_slots == 0) return EAAS_OK;
-  if (!slots || !layers || (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3))
+  if (!slots || !layers ||
+      (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3 && w_dtype != EAAS_FP8_E4M3_A8))
     return EAAS_ERR_INVALID_ARG;
-  const WsLayout L = layout(g);
+  const WsLayout L = layout(g, w_dtype);
   const SlotLayout SL = slot_layout(L.seg_total);
   if (!ws || !aligned16(ws) || ws_bytes < SL.total) return EAAS_ERR_WORKSPACE;
   char* base = static_cast<char*>(ws);
@@ -450,14 +451,15 @@ int eaas_server_step(const eaas_shape* s, const eaas_slot* slots, int n_slots,
     a.perm = rt.perm;
     a.offsets = rt.offsets;
     a.active = rt.active;
-    a.fp8 = w_dtype == EAAS_FP8_E4M3;
+    set_dtype_args(a, w_dtype, base, L);
     a.h = reinterpret_cast<uint16_t*>(base + L.h);
     a.y = reinterpret_cast<float*>(base + L.stage);
     a.topk_weights = w_cat;
     a.epilogue = kDownWeighted;
     a.layers = layers;
     a.e_layer = s->E;
-    e = launch_gate_up(a, hs);
+    e = quantize_x(a, base, L, hs);
+    if (e == hipSuccess) e = launch_gate_up(a, hs);
     if (e == hipSuccess) e = launch_down(a, hs);
     if (e == hipSuccess)
       e = launch_seg_combine(segs, counts, n_slots, cap, g.H, g.k, a.y, rt.inv, false, hs);

@@ -284,16 +284,17 @@ def segment_table(segments, device="cuda") -> torch.Tensor:
 def eaas_expert_forward_segments(table: torch.Tensor, num_tokens: torch.Tensor, n_seg: int,
                                  capacity: int, k: int, w_gate_up: torch.Tensor,
                                  w_down: torch.Tensor, ws: torch.Tensor, out_dtype=EAAS_BF16,
-                                 w_gate_up_scale=None, w_down_scale=None, stream=None) -> None:
+                                 w_gate_up_scale=None, w_down_scale=None, stream=None,
+                                 act8: bool = False) -> None:
     """The step on a dynamic batch: `table` from segment_table, `num_tokens`
     a device int32 tensor of the requests' token counts (read on the device),
-    `capacity` the bound on their sum."""
+    `capacity` the bound on their sum.  act8: fp8 activations."""
     E, twoI, H = w_gate_up.shape
     s = _shape(capacity, H, twoI // 2, E, k)
     st = lib().eaas_expert_forward_segments(
         ctypes.byref(s), _p(table), _p(num_tokens), int(n_seg), _p(w_gate_up),
-        _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up), int(out_dtype),
-        _p(ws), ws.numel(), _stream(stream))
+        _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8),
+        int(out_dtype), _p(ws), ws.numel(), _stream(stream))
     _check(st, "eaas_expert_forward_segments")
 
 

@@ -204,11 +204,15 @@ def test_fp8_activation_mode_host_validation():
 
     assert fwd(sgu=None) == -1            # fp8 weights need their scales
     assert fwd(sh=shape(H=384)) == -2     # H not a multiple of 256
-    # the batched entry points do not take fp8 activations
-    assert L.eaas_segments_workspace_bytes(ctypes.byref(s), A8) == 0
-    assert L.eaas_server_workspace_bytes(ctypes.byref(s), 1, A8) == 0
-    assert L.eaas_expert_forward_segments(ctypes.byref(s), FAKE, FAKE, 1, FAKE, FAKE, FAKE, FAKE,
-                                          A8, 0, FAKE, big, None) == -2
+    # the batched entry points take fp8 activations with the same limits
+    assert L.eaas_segments_workspace_bytes(ctypes.byref(s), A8) > na8
+    assert L.eaas_server_workspace_bytes(ctypes.byref(s), 2, A8) > 0
+    bad = shape(H=384)
+    assert L.eaas_segments_workspace_bytes(ctypes.byref(bad), A8) == 0
+    assert L.eaas_server_workspace_bytes(ctypes.byref(bad), 1, A8) == 0
+    assert L.eaas_expert_forward_segments(ctypes.byref(bad), FAKE, FAKE, 1, FAKE, FAKE, FAKE,
+                                          FAKE, A8, 0, FAKE, big, None) == -2
+    assert L.eaas_server_step(ctypes.byref(bad), FAKE, 1, FAKE, 1, A8, FAKE, big, None) == -2
 
 
 def test_quantize_rows_rejects_bad_args():

@@ -53,7 +53,13 @@ def payload(r):
             torch.from_numpy(np.ascontiguousarray(r["topk_weights"])).cuda())
 
 
-def run_segments(d, reqs, capacity, out_dtype=torch.float32, in_place=False):
+def _wdt(d, act8):
+    if d["wdtype"] != "fp8":
+        return eaas.EAAS_BF16
+    return eaas.EAAS_FP8_E4M3_A8 if act8 else eaas.EAAS_FP8_E4M3
+
+
+def run_segments(d, reqs, capacity, out_dtype=torch.float32, in_place=False, act8=False):
     """Device buffers for every request, then one segments call."""
     dev = to_device(d)
     bufs = []
@@ -66,17 +72,16 @@ def run_segments(d, reqs, capacity, out_dtype=torch.float32, in_place=False):
         bufs.append((x, ids, w, out))
     table = eaas.segment_table(bufs)
     counts = torch.tensor([r["n"] for r in reqs], dtype=torch.int32, device="cuda")
-    wdt = eaas.EAAS_FP8_E4M3 if d["wdtype"] == "fp8" else eaas.EAAS_BF16
-    ws = eaas.alloc_segments_workspace(capacity, d["H"], d["I"], d["E"], d["k"], wdt)
+    ws = eaas.alloc_segments_workspace(capacity, d["H"], d["I"], d["E"], d["k"], _wdt(d, act8))
     odt = eaas.EAAS_FP32 if (out_dtype == torch.float32 and not in_place) else eaas.EAAS_BF16
     eaas.eaas_expert_forward_segments(table, counts, len(reqs), capacity, d["k"], dev["w_gate_up"],
                                       dev["w_down"], ws, odt, dev["w_gate_up_scale"],
-                                      dev["w_down_scale"])
+                                      dev["w_down_scale"], act8=act8)
     torch.cuda.synchronize()
     return bufs, dict(table=table, counts=counts, ws=ws, dev=dev, odt=odt)
 
 
-def forward_concat(d, reqs, out_dtype=torch.float32, limit=None):
+def forward_concat(d, reqs, out_dtype=torch.float32, limit=None, act8=False):
     """eaas_expert_forward on the requests concatenated in slot order."""
     cat = S.dynamic_batch(reqs)
     if limit is not None:
@@ -84,11 +89,11 @@ def forward_concat(d, reqs, out_dtype=torch.float32, limit=None):
     if cat["T"] == 0:
         return np.zeros((0, d["H"]))
     dev = to_device(cat)
-    wdt = eaas.EAAS_FP8_E4M3 if d["wdtype"] == "fp8" else eaas.EAAS_BF16
-    ws = eaas.alloc_workspace(cat["T"], d["H"], d["I"], d["E"], d["k"], wdt)
+    ws = eaas.alloc_workspace(cat["T"], d["H"], d["I"], d["E"], d["k"], _wdt(d, act8))
     out = torch.empty((cat["T"], d["H"]), dtype=out_dtype, device="cuda")
     eaas.eaas_expert_forward(dev["x"], dev["topk_ids"], dev["topk_weights"], dev["w_gate_up"],
-                             dev["w_down"], out, ws, dev["w_gate_up_scale"], dev["w_down_scale"])
+                             dev["w_down"], out, ws, dev["w_gate_up_scale"], dev["w_down_scale"],
+                             act8=act8)
     torch.cuda.synchronize()
     return out
 
@@ -137,6 +142,17 @@ def test_segments_fp8_many_clients(gpu):
     bufs, _ = run_segments(d, reqs, 256)
     check_against(reqs, bufs, forward_concat(d, reqs))
     check_oracle(reqs, bufs)
+
+
+def test_segments_fp8_activations(gpu):
+    # fp8 activations: x and h are quantized per row, so each request's rows
+    # still equal the concatenated step's bit for bit
+    rng = np.random.default_rng(11)
+    sizes = [int(v) for v in rng.integers(0, 40, size=12)]
+    d, reqs = make_requests(sizes, H=512, I=256, E=16, k=4, seed=44, wdtype="fp8")
+    say("segments fp8 activations", sum(sizes))
+    bufs, _ = run_segments(d, reqs, 512, act8=True)
+    check_against(reqs, bufs, forward_concat(d, reqs, act8=True))
 
 
 def test_segments_capacity_cuts_the_batch(gpu):

@@ -52,9 +52,11 @@ def make_slots(specs, seed=70):
 class Server:
     """Device-resident slots and layer weights, as a server would hold them."""
 
-    def __init__(self, slots, layers, capacity):
-        self.slots, self.layers, self.cap = slots, layers, capacity
+    def __init__(self, slots, layers, capacity, act8=False):
+        self.slots, self.layers, self.cap, self.act8 = slots, layers, capacity, act8
         self.wdt = eaas.EAAS_FP8_E4M3 if layers[0]["wdtype"] == "fp8" else eaas.EAAS_BF16
+        if act8:
+            self.wdt = eaas.EAAS_FP8_E4M3_A8
         self.dl = [to_device(dict(lw, x=np.zeros((1, H), np.uint16),
                                   topk_ids=np.zeros((1, K), np.int32),
                                   topk_weights=np.zeros((1, K), np.float32))) for lw in layers]
@@ -86,7 +88,7 @@ class Server:
         self.dev[b][0].fill_(flag)
 
 
-def forward_layer_concat(slots, members, counts, lw):
+def forward_layer_concat(slots, members, counts, lw, act8=False):
     """eaas_expert_forward (bf16 out) on the given requests concatenated."""
     T = int(sum(counts[b] for b in members))
     d = dict(lw, T=T, H=H, I=I, E=E, k=K,
@@ -95,10 +97,13 @@ def forward_layer_concat(slots, members, counts, lw):
              topk_weights=np.concatenate([slots[b]["topk_weights"][: counts[b]] for b in members]))
     dev = to_device(d)
     wdt = eaas.EAAS_FP8_E4M3 if lw["wdtype"] == "fp8" else eaas.EAAS_BF16
+    if act8:
+        wdt = eaas.EAAS_FP8_E4M3_A8
     ws = eaas.alloc_workspace(T, H, I, E, K, wdt)
     out = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
     eaas.eaas_expert_forward(dev["x"], dev["topk_ids"], dev["topk_weights"], dev["w_gate_up"],
-                             dev["w_down"], out, ws, dev["w_gate_up_scale"], dev["w_down_scale"])
+                             dev["w_down"], out, ws, dev["w_gate_up_scale"], dev["w_down_scale"],
+                             act8=act8)
     torch.cuda.synchronize()
     return bf16_tensor_to_bits(out)
 
@@ -120,15 +125,16 @@ def check_step(srv, before):
         members = [b for b in range(len(before)) if taken[b] and before[b]["layer"] == L and counts[b]]
         if not members:
             continue
-        ref = forward_layer_concat(before, members, counts, lw)
+        ref = forward_layer_concat(before, members, counts, lw, srv.act8)
         p = 0
         for b in members:
             n = int(counts[b])
             assert np.array_equal(xs[b][:n], ref[p:p + n]), f"slot {b} vs concatenated forward"
-            got = (xs[b][:n].astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-            rms = float(np.sqrt((want_res[b] ** 2).mean()))
-            # bf16 output: one rounding of the result on top of the fp32 budget
-            assert np.abs(got - want_res[b]).max() <= TOL * rms + np.abs(want_res[b]).max() * 2 ** -8
+            if not srv.act8:  # (the fp8-activation step has its own oracle and tests)
+                got = (xs[b][:n].astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+                rms = float(np.sqrt((want_res[b] ** 2).mean()))
+                # bf16 output: one rounding of the result on top of the fp32 budget
+                assert np.abs(got - want_res[b]).max() <= TOL * rms + np.abs(want_res[b]).max() * 2 ** -8
             p += n
     for b, s in enumerate(before):
         if taken[b] and counts[b] and not (0 <= s["layer"] < len(srv.layers)):
@@ -170,6 +176,17 @@ def test_server_step_fp8_three_layers(gpu):
     slots = make_slots(specs, seed=71)
     srv = Server(slots, layers, capacity=256)
     say("server step fp8, 3 layers")
+    before = snapshot(srv.slots)
+    srv.step()
+    check_step(srv, before)
+
+
+def test_server_step_fp8_activations(gpu):
+    layers = make_layers(2, wdtype="fp8", seed=63)
+    specs = [(1, L % 2, n, n + 3) for L, n in enumerate([21, 8, 40, 0, 13, 64])]
+    slots = make_slots(specs, seed=73)
+    srv = Server(slots, layers, capacity=256, act8=True)
+    say("server step fp8 activations, 2 layers")
     before = snapshot(srv.slots)
     srv.step()
     check_step(srv, before)
