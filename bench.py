@@ -362,8 +362,13 @@ def main() -> int:
 
     t_route, t_gu, t_dn, t_comb = mean_ms(0, 1), mean_ms(1, 2), mean_ms(2, 3), mean_ms(3, 4)
     t_step_ev = mean_ms(0, 4)
-    hbm_bound = d["wdtype"] == "fp8" and not act8
-    if act8:
+    # the gate/up launch's bound: HBM when its algorithmic intensity is below
+    # the ridge of the MFMA peak it runs on (fp8 x fp8 with fp8 activations,
+    # bf16 otherwise), the matrix cores above it
+    peak_flops = PEAK_FP8_TFLOPS if act8 else PEAK_BF16_TFLOPS
+    intensity = alg["gu_flops"] / alg["gu_bytes"]
+    hbm_bound = intensity < peak_flops * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if act8 and not hbm_bound:
         # fp8 x fp8 contraction: priced against the fp8 MFMA peak
         achieved = alg["gu_flops"] / (t_gu * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_FP8_TFLOPS,

@@ -65,9 +65,11 @@ WORKLOADS = {
     "qwen3": Workload("qwen3", 8192, 2048, 768, 128, 8, 2, zipf=1.1),
     "dsv3_prefill": Workload("dsv3_prefill", 16384, 7168, 2048, 32, 8, 3, zipf=1.2),
     "dsv3_decode": Workload("dsv3_decode", 256, 7168, 2048, 32, 8, 4, wdtype="fp8"),
-    # dsv3_prefill's batch and routing with fp8 weights and fp8 activations
+    # dsv3_prefill's and dsv3_decode's batches with fp8 weights and fp8 activations
     "dsv3_prefill_w8a8": Workload("dsv3_prefill_w8a8", 16384, 7168, 2048, 32, 8, 3, zipf=1.2,
                                   wdtype="fp8", act8=True),
+    "dsv3_decode_w8a8": Workload("dsv3_decode_w8a8", 256, 7168, 2048, 32, 8, 4, wdtype="fp8",
+                                 act8=True),
 }
 
 
