@@ -52,7 +52,7 @@ def gate_up_kernel_name(d: dict) -> str:
         return "grouped_gemm_w8a8_kernel<gate/up>"
     if d["wdtype"] == "fp8":
         return "grouped_gemm_dma_kernel<gate/up, fp8 weights>"
-    if T * k <= 128 * E or (2 * I) % 256:
+    if (2 * I) % 256:
         return "grouped_gemm_kernel<gate/up, register-staged>"
     return "grouped_gemm_pp_kernel<gate/up>"
 

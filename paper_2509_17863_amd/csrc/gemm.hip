@@ -27,7 +27,7 @@
 //     each 128-wide K block's MFMA partial sum is scaled and added to the
 //     fp32 accumulator (grouped_gemm_dma_kernel).
 // A register-staged loop covers shapes the DMA tiles do not (N not a multiple
-// of 256, decode-sized bf16 batches).
+// of 256).
 // LDS rows are BK elements long; 16-byte chunk c of row r is stored at chunk
 // c ^ swz(r) so 32-row fragment reads hit every bank once.
 //
@@ -1462,7 +1462,7 @@ hipError_t launch_w8a8(const GemmParams& p, int R, int E, hipStream_t stream) {
 //     MFMAs -- BK=64, 2 token-row stages and 4 weight stages (152 KiB), so
 //     96 KiB of weights per CU are in flight while a tile is multiplied
 //     (96x256 with 4 waves and 3+3 stages when N is not a multiple of 512);
-//   decode-sized bf16 and other N: register-staged 128-row tiles.
+//   N not a multiple of 256: register-staged 128-row tiles.
 template <int KIND, bool FP8>
 hipError_t launch_kind(const GemmParams& p, int R, int E, bool small_m, hipStream_t stream) {
   const bool n256 = (p.N % 256) == 0;
@@ -1472,11 +1472,10 @@ hipError_t launch_kind(const GemmParams& p, int R, int E, bool small_m, hipStrea
     if (small_m) return launch_reg<KIND, true, 1, 2, 4, 2>(p, R, E, stream);
     return launch_reg<KIND, true, 2, 2, 4, 2>(p, R, E, stream);
   } else {
-    if (small_m) {
-      if (n256) return launch_reg<KIND, false, 1, 4, 4, 2>(p, R, E, stream);
-      return launch_reg<KIND, false, 1, 2, 4, 2>(p, R, E, stream);
-    }
+    // the ping-pong kernel also beats the register-staged loop on
+    // decode-sized batches (its weight stream keeps more bytes in flight)
     if (n256) return launch_pp<KIND>(p, R, E, stream);
+    if (small_m) return launch_reg<KIND, false, 1, 2, 4, 2>(p, R, E, stream);
     return launch_reg<KIND, false, 2, 2, 4, 2>(p, R, E, stream);
   }
 }
