@@ -298,15 +298,16 @@ def test_forward_w8a8_exact_grid(gpu):
     check_step(d, got, ws, np.arange(d["T"]), "w8a8 exact grid")
 
 
-def test_forward_w8a8_workload_sampled(gpu):
-    """dsv3_prefill's shape with fp8 weights and fp8 activations, sampled."""
-    d = synth.make_workload("dsv3_prefill_w8a8")
+@pytest.mark.parametrize("name", [n for n, w in synth.WORKLOADS.items() if w.act8])
+def test_forward_w8a8_workload_sampled(gpu, name):
+    """The fp8-activation workloads at full size, sampled tokens."""
+    d = synth.make_workload(name)
     T = d["T"]
-    say("forward w8a8 workload dsv3_prefill_w8a8")
+    say("forward w8a8 workload", name)
     got, ws = forward_a8(d)
     rng = np.random.default_rng(4321)
-    tokens = np.sort(rng.choice(T, size=32, replace=False))
-    check_step(d, got, ws, tokens, "workload dsv3_prefill_w8a8 (32 sampled tokens)")
+    tokens = np.sort(rng.choice(T, size=min(T, 32), replace=False))
+    check_step(d, got, ws, tokens, f"workload {name} ({len(tokens)} sampled tokens)")
 
 
 def test_w8a8_shape_limits(gpu):
