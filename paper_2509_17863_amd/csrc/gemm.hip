@@ -18,14 +18,18 @@
 // Operands go global -> LDS directly (global_load_lds, 16 B per lane, no VGPR
 // staging) through rings of token-row (A) and weight (B) stages; later tiles
 // are in flight while one is multiplied.  Waits are explicit vmcnt counts plus
-// a bare s_barrier.  Two main loops use this:
-//   - bf16 weights, prefill-sized batches: an 8-wave ping-pong in which the
-//     two waves of each SIMD alternate between reading a whole K tile's
-//     fragments from LDS and issuing its MFMAs (grouped_gemm_pp_kernel);
-//   - fp8-e4m3 weights (one fp32 scale per 128x128 block): the weights stay
-//     fp8 in LDS and are converted to bf16 (exactly) as fragments are read;
-//     each 128-wide K block's MFMA partial sum is scaled and added to the
-//     fp32 accumulator (grouped_gemm_dma_kernel).
+// a bare s_barrier.  Three main loops use this:
+//   - bf16 weights: an 8-wave ping-pong in which the two waves of each SIMD
+//     alternate between reading a whole K tile's fragments from LDS and
+//     issuing its MFMAs (grouped_gemm_pp_kernel);
+//   - fp8-e4m3 weights (one fp32 scale per 128x128 block) with bf16
+//     activations: the weights stay fp8 in LDS and are converted to bf16
+//     (exactly) as fragments are read; each 128-wide K block's MFMA partial
+//     sum is scaled and added to the fp32 accumulator
+//     (grouped_gemm_dma_kernel);
+//   - fp8 weights with fp8 activations (one fp32 scale per row and 128
+//     channels): a ping-pong on block-scaled fp8 MFMAs, promoting every K
+//     tile (grouped_gemm_w8a8_kernel).
 // A register-staged loop covers shapes the DMA tiles do not (N not a multiple
 // of 256).
 // LDS rows are BK elements long; 16-byte chunk c of row r is stored at chunk
