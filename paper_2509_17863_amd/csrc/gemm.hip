@@ -330,6 +330,69 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, const Tile& t, int
   }
 }
 
+// Down projection epilogue through LDS.  In the MFMA layout a store
+// instruction writes 32-byte pieces of 32 different rows (lanes l and l+32
+// hold neighbouring 4-column runs of token row l%32), and the fp32 staging
+// rows of a down tile are scattered slots: the stores then cost more than
+// the tile's last K tiles.  Here each wave passes its accumulators, one
+// 32-row block at a time, through a private LDS region and stores whole
+// rows of its columns: with NBW = 2 one instruction writes 4 rows x 256
+// contiguous bytes.  The values stored are those of `epilogue` (the same
+// rounded product w * a, or a), bit for bit.  Every wave must have finished
+// the main loop's LDS reads (and its DMA must have landed) before any wave
+// calls this: the callers reach it after the loop's last barrier.
+template <int NBW>
+constexpr int kRowsLdsBytes = 32 * (NBW * 32 + 4) * 4;  // one wave's region
+
+template <int KIND, int BN, int MBW, int NBW>
+__device__ __forceinline__ void epilogue_rows_lds(const GemmParams& p, const Tile& t, int wn,
+                                                  int am0, int mb_live, const RowInfo<MBW>& ri,
+                                                  const f32x16 (&acc)[MBW][NBW],
+                                                  LDS_AS float* buf) {
+  static_assert(KIND != kGateUp, "down projection only");
+  constexpr int COLS = NBW * 32;     // the wave's columns
+  constexpr int LD = COLS + 4;       // LDS row stride in floats: 16-byte pad against bank conflicts
+  constexpr int LPR = COLS / 4;      // lanes per row when reading 16 bytes each
+  constexpr int RPI = kWave / LPR;   // rows per read / store instruction
+  static_assert(LPR * 4 == COLS && RPI * LPR == kWave && 32 % RPI == 0, "row layout");
+  // the lane id from mbcnt, so that threadIdx need not stay live through the loop
+  const int lane = __lane_id();
+  const int lrow = lane & 31;
+  const int khalf = lane >> 5;
+  const int rl = lane / LPR;
+  const int cl = (lane % LPR) * 4;
+  float* ybase = p.y + t.tn * BN + wn * COLS + cl;
+#pragma unroll
+  for (int i = 0; i < MBW; ++i) {
+    if (i >= mb_live) continue;
+    const float wt = ri.wt[i];
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        f32x4 v;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float a = acc[i][j][4 * q + u];
+          v[u] = KIND == kDownWeightedK ? wt * a : a;  // rounded product, stored
+        }
+        *reinterpret_cast<LDS_AS f32x4*>(buf + lrow * LD + j * 32 + 8 * q + 4 * khalf) = v;
+      }
+    }
+    // a wave's LDS operations complete in order: the reads below see the
+    // writes above, and the next block's writes follow these reads
+#pragma unroll
+    for (int s = 0; s < 32 / RPI; ++s) {
+      const int m = s * RPI + rl;
+      const f32x4 v = *reinterpret_cast<const LDS_AS f32x4*>(buf + m * LD + cl);
+      const int orow = __shfl(ri.orow[i], m);  // lane m holds row m's destination
+      // non-temporal: the combine reads the staging once, after this launch
+      if (am0 + i * 32 + m < t.rows_valid)
+        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(ybase + (size_t)orow * p.N));
+    }
+  }
+}
+
 // ============================================================================
 // bf16 weights: LDS-DMA ring
 // ============================================================================
@@ -719,7 +782,16 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   else
     Part::run(smem, src, nk, a_lane_off, b_lane_off, s_l, sb_l, mb_live, sc, acc);
 
-  epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, ri, acc);
+  if constexpr (GATEUP) {
+    epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, ri, acc);
+  } else {
+    // the last K tile ends without a barrier: every wave's fragment reads
+    // must be done before the epilogue regions overwrite the stages
+    static_assert(NW * kRowsLdsBytes<NBW> <= Full::LDS_BYTES, "epilogue regions");
+    __syncthreads();
+    epilogue_rows_lds<KIND, BN, MBW, NBW>(
+        p, t, wn, am0, mb_live, ri, acc, (LDS_AS float*)(smem_raw + wave * kRowsLdsBytes<NBW>));
+  }
 }
 
 // ============================================================================
@@ -1123,7 +1195,14 @@ void grouped_gemm_pp_kernel(GemmParams p) {
   // the epilogue's row information is loaded only now: a vector load in
   // the loop would make the compiler wait for vmcnt(0) there
   const RowInfo<MBW> ri = row_info<KIND, MBW>(p, t, am0, mb_live);
-  epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, ri, acc);
+  if constexpr (GATEUP) {
+    epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, ri, acc);
+  } else {
+    static_assert(8 * kRowsLdsBytes<NBW> <= LDS_BYTES, "epilogue regions");
+    epilogue_rows_lds<KIND, BN, MBW, NBW>(
+        p, t, wn, am0, mb_live, ri, acc,
+        (LDS_AS float*)(smem_raw + wave * kRowsLdsBytes<NBW>));
+  }
 }
 
 template <int KIND>
@@ -1443,8 +1522,11 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
       if (wn == 0 && khalf == 0) p.hs[(size_t)r * nkh + t.tn] = s;
     }
   } else {
+    // after the loop's last barrier: no wave reads the stages any more
     const RowInfo<MBW> ri = row_info<KIND, MBW>(p, t, am0, mb_live);
-    epilogue<KIND, BN, MBW, NBW>(p, t, wn, am0, mb_live, ri, acc);
+    static_assert(8 * kRowsLdsBytes<NBW> <= LDS_BYTES, "epilogue regions");
+    epilogue_rows_lds<KIND, BN, MBW, NBW>(
+        p, t, wn, am0, mb_live, ri, acc, (LDS_AS float*)(smem_raw + wave * kRowsLdsBytes<NBW>));
   }
 }
 
