@@ -688,9 +688,12 @@ struct DmaLoop {
   }
 };
 
-template <int KIND, bool FP8, int BK, int SA, int SB, int BSPAN, int WM, int WN, int MBW, int NBW>
+// OCC: workgroups per CU the launch is sized for (the LDS footprint must
+// allow it); it sets the waves per SIMD the registers are budgeted for.
+template <int KIND, bool FP8, int BK, int SA, int SB, int BSPAN, int WM, int WN, int MBW, int NBW,
+          int OCC>
 __global__ __launch_bounds__(WM * WN * kWave)
-__attribute__((amdgpu_waves_per_eu(WM * WN / 4, WM * WN / 4)))
+__attribute__((amdgpu_waves_per_eu(WM * WN * OCC / 4, WM * WN * OCC / 4)))
 void grouped_gemm_dma_kernel(GemmParams p) {
   constexpr int NW = WM * WN;
   constexpr int NT = NW * kWave;
@@ -989,13 +992,16 @@ hipError_t launch_reg(const GemmParams& p, int R, int E, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int KIND, bool FP8, int BK, int SA, int SB, int BSPAN, int WM, int WN, int MBW, int NBW>
+template <int KIND, bool FP8, int BK, int SA, int SB, int BSPAN, int WM, int WN, int MBW, int NBW,
+          int OCC = 1>
 hipError_t launch_dma(const GemmParams& p, int R, int E, hipStream_t stream) {
   constexpr int BM = WM * MBW * 32, BN = WN * NBW * 32;
+  using Loop = DmaLoop<KIND, BK, SA, SB, BSPAN, WM * WN, BM, BN, MBW, NBW, true, FP8>;
+  static_assert(OCC * Loop::LDS_BYTES <= 160 * 1024 - OCC * 1024, "workgroups per CU must fit in LDS");
   const long long grid = grid_tiles(R, E, BM, BN, p.N);
   if (grid <= 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((grouped_gemm_dma_kernel<KIND, FP8, BK, SA, SB, BSPAN, WM, WN, MBW, NBW>),
+  hipLaunchKernelGGL((grouped_gemm_dma_kernel<KIND, FP8, BK, SA, SB, BSPAN, WM, WN, MBW, NBW, OCC>),
                      dim3((unsigned)grid), dim3(WM * WN * kWave), 0, stream, p);
   return hipGetLastError();
 }
@@ -1553,8 +1559,15 @@ template <int KIND, bool FP8>
 hipError_t launch_kind(const GemmParams& p, int R, int E, bool small_m, hipStream_t stream) {
   const bool n256 = (p.N % 256) == 0;
   if constexpr (FP8) {
-    if (p.N % 512 == 0) return launch_dma<KIND, true, 64, 2, 4, 1, 1, 8, 3, 2>(p, R, E, stream);
-    if (n256) return launch_dma<KIND, true, 64, 3, 3, 1, 1, 4, 3, 2>(p, R, E, stream);
+    // the down projection runs two 4-wave workgroups of 96x256 per CU: twice
+    // the tiles of the 512-wide layout (a shorter tail), and two independent
+    // barrier domains per CU
+    if constexpr (KIND != kGateUp) {
+      if (n256) return launch_dma<KIND, true, 64, 2, 3, 1, 1, 4, 3, 2, 2>(p, R, E, stream);
+    } else {
+      if (p.N % 512 == 0) return launch_dma<KIND, true, 64, 2, 4, 1, 1, 8, 3, 2>(p, R, E, stream);
+      if (n256) return launch_dma<KIND, true, 64, 3, 3, 1, 1, 4, 3, 2>(p, R, E, stream);
+    }
     if (small_m) return launch_reg<KIND, true, 1, 2, 4, 2>(p, R, E, stream);
     return launch_reg<KIND, true, 2, 2, 4, 2>(p, R, E, stream);
   } else {
