@@ -11,6 +11,8 @@
 //                  quarter of it: ranks equal ids inside the wave with ballot
 //                  matching, so row = offsets[e] + (earlier chunks) + (earlier
 //                  waves) + (earlier steps) + (earlier lanes): stable by slot.
+//   route_fused    batches of at most two chunks: the same three steps in one
+//                  workgroup (decode sizes, where the launches dominate).
 //
 // No floating point and no order-dependent atomics: results are bit-exact.
 #include "common.h"
@@ -167,6 +169,94 @@ __global__ __launch_bounds__(kRouteThreads) void route_scatter_kernel(
   for (int r = rbeg + tid; r < rend; r += kRouteThreads) perm[r] = -1;
 }
 
+// Small batches (R <= kFusedMaxSlots, decode sizes): the three steps in one
+// workgroup of 16 waves, with barriers where the separate kernels have
+// launch boundaries.  Wave w owns the contiguous slots [w*sub, (w+1)*sub);
+// its per-expert counts, turned into starting rows, play the part of the
+// per-chunk histogram, so the ranks (and perm, inv) are those of the
+// three-kernel path: stable by slot.
+constexpr int kFusedWaves = kScanThreads / kWave;
+constexpr int kFusedMaxSlots = 2 * kRouteChunk;
+
+__global__ __launch_bounds__(kScanThreads) void route_fused_kernel(
+    const int32_t* __restrict__ ids, int R, int E, int nbits, int32_t* __restrict__ counts,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ active, int32_t* __restrict__ perm,
+    int32_t* __restrict__ inv) {
+  __shared__ int next[kFusedWaves * kMaxExperts];  // [w][e], counts then starting rows
+  __shared__ int s_wave[kScanThreads / kWave + 1];
+  __shared__ int s_act[kMaxExperts];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = tid / kWave;
+  for (int i = tid; i < kFusedWaves * E; i += kScanThreads) next[(i / E) * kMaxExperts + i % E] = 0;
+  __syncthreads();
+  const int sub = (R + kFusedWaves * kWave - 1) / (kFusedWaves * kWave) * kWave;
+  const int s0 = wave * sub;
+  const int s1 = min(s0 + sub, R);
+  int* mine = next + wave * kMaxExperts;
+  for (int s = s0 + lane; s < s1; s += kWave) {
+    const int id = ids[s];
+    if ((unsigned)id < (unsigned)E) atomicAdd(&mine[id], 1);
+  }
+  __syncthreads();
+  // thread e: the expert's count, its offset and the compacted active list
+  const int e = tid;  // E <= 1024 = blockDim
+  int c = 0;
+  if (e < E) {
+    for (int w = 0; w < kFusedWaves; ++w) c += next[w * kMaxExperts + e];
+  }
+  int valid_total;
+  const int off = block_exclusive_scan_1024(c, s_wave, &valid_total);
+  int n_active;
+  const int apos = block_exclusive_scan_1024((e < E && c > 0) ? 1 : 0, s_wave, &n_active);
+  if (e < E && c > 0) s_act[apos] = e;
+  if (e < E) {
+    int a = off;
+    for (int w = 0; w < kFusedWaves; ++w) {
+      const int cw = next[w * kMaxExperts + e];
+      next[w * kMaxExperts + e] = a;
+      a += cw;
+    }
+  }
+  __syncthreads();
+  if (e < E) {
+    counts[e] = c;
+    offsets[e] = off;
+    active[1 + e] = e < n_active ? s_act[e] : 0;
+  }
+  if (e == 0) {
+    offsets[E] = valid_total;
+    active[0] = n_active;
+  }
+  // stable ranks, 64 slots per step, steps in slot order (as route_scatter)
+  const uint64_t lt = lanemask_lt();
+  for (int i = s0; i < s0 + sub; i += kWave) {
+    const int s = i + lane;
+    const int id = s < s1 ? ids[s] : -1;
+    const bool valid = (unsigned)id < (unsigned)E;
+    uint64_t peers = ballot(valid);
+    for (int b = 0; b < nbits; ++b) {
+      const bool bit = (id >> b) & 1;
+      const uint64_t m = ballot(bit);
+      peers &= bit ? m : ~m;
+    }
+    int rank = 0;
+    if (valid) {
+      rank = __popcll(peers & lt);
+      const int row = mine[id] + rank;
+      perm[row] = s;
+      inv[s] = row;
+    } else if (s < s1) {
+      inv[s] = -1;
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (valid && rank == 0) mine[id] += __popcll(peers);
+    __builtin_amdgcn_wave_barrier();
+  }
+  // rows past the number of valid slots carry no slot
+  for (int r = valid_total + tid; r < R; r += kScanThreads) perm[r] = -1;
+}
+
 }  // namespace
 
 hipError_t launch_route_permute(const int32_t* ids, int R, int E,
@@ -175,6 +265,11 @@ hipError_t launch_route_permute(const int32_t* ids, int R, int E,
   const int nblk = route_blocks(R);
   int nbits = 1;
   while ((1 << nbits) < E) ++nbits;
+  if (R <= kFusedMaxSlots) {
+    hipLaunchKernelGGL(route_fused_kernel, dim3(1), dim3(kScanThreads), 0, stream, ids, R, E,
+                       nbits, r.counts, r.offsets, r.active, r.perm, r.inv);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(route_hist_kernel, dim3(nblk), dim3(kRouteThreads), 0, stream,
                      ids, R, E, hist);
   hipLaunchKernelGGL(route_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream,

@@ -82,6 +82,8 @@ ROUTE_CASES = [
     (1, 1, 1, 0.0, 0), (3, 8, 2, 0.0, 1), (100, 8, 2, 0.3, 2), (1000, 3, 8, 0.1, 3),
     (2047, 64, 1, 0.0, 4), (2049, 128, 8, 0.05, 5), (513, 1024, 4, 0.0, 6),
     (5000, 1024, 2, 0.5, 7), (300, 5, 5, 0.0, 8),
+    # around the single-workgroup path's limit of 4096 slots
+    (1024, 16, 4, 0.2, 9), (4096, 1024, 1, 0.1, 10), (4097, 7, 1, 0.0, 11), (1, 1024, 8, 0.5, 12),
 ]
 
 
