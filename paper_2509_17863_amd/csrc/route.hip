@@ -11,7 +11,7 @@
 //                  quarter of it: ranks equal ids inside the wave with ballot
 //                  matching, so row = offsets[e] + (earlier chunks) + (earlier
 //                  waves) + (earlier steps) + (earlier lanes): stable by slot.
-//   route_fused    batches of at most two chunks: the same three steps in one
+//   route_fused    batches of at most four chunks: the same three steps in one
 //                  workgroup (decode sizes, where the launches dominate).
 //
 // No floating point and no order-dependent atomics: results are bit-exact.
@@ -169,14 +169,14 @@ __global__ __launch_bounds__(kRouteThreads) void route_scatter_kernel(
   for (int r = rbeg + tid; r < rend; r += kRouteThreads) perm[r] = -1;
 }
 
-// Small batches (R <= kFusedMaxSlots, decode sizes): the three steps in one
+// Small batches (R <= kFusedMaxSlots = 8192): the three steps in one
 // workgroup of 16 waves, with barriers where the separate kernels have
 // launch boundaries.  Wave w owns the contiguous slots [w*sub, (w+1)*sub);
 // its per-expert counts, turned into starting rows, play the part of the
 // per-chunk histogram, so the ranks (and perm, inv) are those of the
 // three-kernel path: stable by slot.
 constexpr int kFusedWaves = kScanThreads / kWave;
-constexpr int kFusedMaxSlots = 2 * kRouteChunk;
+constexpr int kFusedMaxSlots = 4 * kRouteChunk;
 
 __global__ __launch_bounds__(kScanThreads) void route_fused_kernel(
     const int32_t* __restrict__ ids, int R, int E, int nbits, int32_t* __restrict__ counts,

@@ -82,8 +82,9 @@ ROUTE_CASES = [
     (1, 1, 1, 0.0, 0), (3, 8, 2, 0.0, 1), (100, 8, 2, 0.3, 2), (1000, 3, 8, 0.1, 3),
     (2047, 64, 1, 0.0, 4), (2049, 128, 8, 0.05, 5), (513, 1024, 4, 0.0, 6),
     (5000, 1024, 2, 0.5, 7), (300, 5, 5, 0.0, 8),
-    # around the single-workgroup path's limit of 4096 slots
-    (1024, 16, 4, 0.2, 9), (4096, 1024, 1, 0.1, 10), (4097, 7, 1, 0.0, 11), (1, 1024, 8, 0.5, 12),
+    # around the single-workgroup path's limit of 8192 slots
+    (1024, 16, 4, 0.2, 9), (8192, 1024, 1, 0.1, 10), (8193, 7, 1, 0.0, 11), (1, 1024, 8, 0.5, 12),
+    (4096, 8, 2, 0.0, 13),
 ]
 
 
@@ -125,6 +126,7 @@ SMALL = [
     (1, 256, 128, 4, 2, 24, None, "bf16", 0.0),      # single token
     (130, 512, 256, 4, 3, 25, None, "fp8", 0.0),     # fp8 block-scaled weights
     (600, 768, 512, 3, 2, 26, None, "fp8", 0.2),     # fp8, several tiles, masked
+    (200, 384, 384, 5, 2, 27, 1.5, "fp8", 0.1),      # fp8, gate/up N = 768, down N = 384
 ]
 
 
