@@ -1147,7 +1147,10 @@ void grouped_gemm_pp_kernel(GemmParams p) {
       // the stage may be refilled right after the next barrier
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     };
+    // the C phase runs at raised wave priority: its MFMAs win the SIMD's
+    // issue arbitration against the other group's fragment reads and DMA
     auto mfmas = [&]() {
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk)
 #pragma unroll
@@ -1157,6 +1160,7 @@ void grouped_gemm_pp_kernel(GemmParams p) {
             for (int j = 0; j < NBW; ++j)
               acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[kk][j], fa[kk][i],
                                                                   acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_s_setprio(0);
     };
 
     // prologue: each group's first two K tiles of its operand; tile 0 must
@@ -1427,7 +1431,9 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
   // C(kt): the tile's MFMAs into `part`; before each block's first MFMA, the
   // previous tile's partial sums of that block are promoted (VALU work that
   // runs beside the matrix pipe)
+  // the C phase runs at raised wave priority, as in the bf16 ping-pong
   auto mfmas = [&]() {
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int i = 0; i < MBW; ++i)
 #pragma unroll
@@ -1441,6 +1447,7 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
     for (int i = 0; i < MBW; ++i)
 #pragma unroll
       for (int j = 0; j < NBW; ++j) part[i][j] = mma(fb[1][j], fa[1][i], part[i][j]);
+    __builtin_amdgcn_s_setprio(0);
   };
 
   // prologue: each group's first two K tiles of its operand; tile 0 must
