@@ -38,11 +38,16 @@ def algorithmic(d: dict, counts: np.ndarray) -> dict:
     wb = 1 if d["wdtype"] == "fp8" else 2
     sgu = (2 * I // 128) * (H // 128) * 4 if wb == 1 else 0
     sdn = (H // 128) * (I // 128) * 4 if wb == 1 else 0
-    gu_bytes = n_act * (2 * I * H * wb + sgu) + T * H * 2 + R * I * 2 + R * 4
-    dn_bytes = n_act * (H * I * wb + sdn) + R * I * 2 + T * H * 2 + R * 4
+    if d.get("act8"):
+        # fp8 activations: x and h enter the GEMMs as e4m3 codes (1 byte) plus
+        # one fp32 scale per row and 128 channels
+        gu_bytes = n_act * (2 * I * H + sgu) + T * H + T * H // 32 + R * I + R * I // 32 + R * 4
+        dn_bytes = n_act * (H * I + sdn) + R * I + R * I // 32 + T * H * 2 + R * 4
+    else:
+        gu_bytes = n_act * (2 * I * H * wb + sgu) + T * H * 2 + R * I * 2 + R * 4
+        dn_bytes = n_act * (H * I * wb + sdn) + R * I * 2 + T * H * 2 + R * 4
     return dict(flops=6.0 * R * H * I, gu_flops=4.0 * R * H * I, dn_flops=2.0 * R * H * I,
-                gu_bytes=gu_bytes, dn_bytes=dn_bytes,
-                bytes=gu_bytes + dn_bytes - R * I * 2 * 0 + T * k * 4)
+                gu_bytes=gu_bytes, dn_bytes=dn_bytes, bytes=gu_bytes + dn_bytes + T * k * 4)
 
 
 def gate_up_kernel_name(d: dict) -> str:
