@@ -275,6 +275,49 @@ def test_graph_replay_matches_eager(gpu):
         assert np.array_equal(out.cpu().numpy().view(np.uint32), eager.view(np.uint32)), i
 
 
+def test_concurrent_streams_are_independent(gpu):
+    """The library keeps no state between calls: two forwards of different
+    batches in flight at once on two streams (own workspaces) give the
+    results each gives alone, bit for bit."""
+    da = _mid_inputs(seed=36)
+    db = synth.make_inputs(300, 512, 256, 8, 4, 37, zipf=None, wdtype="fp8")
+    deva, devb = to_device(da), to_device(db)
+    say("concurrent streams")
+    alone_a = forward(deva, da["k"]).cpu().numpy()
+    alone_b = forward(devb, db["k"]).cpu().numpy()
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = []
+    for _ in range(3):
+        oa = torch.full((da["T"], da["H"]), float("nan"), device="cuda")
+        ob = torch.full((db["T"], db["H"]), float("nan"), device="cuda")
+        sa.wait_stream(torch.cuda.current_stream())
+        sb.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(sa):
+            forward(deva, da["k"], out=oa, stream=sa.cuda_stream)
+        with torch.cuda.stream(sb):
+            forward(devb, db["k"], out=ob, stream=sb.cuda_stream)
+        outs.append((oa, ob))
+    torch.cuda.synchronize()
+    for oa, ob in outs:
+        assert np.array_equal(oa.cpu().numpy().view(np.uint32), alone_a.view(np.uint32))
+        assert np.array_equal(ob.cpu().numpy().view(np.uint32), alone_b.view(np.uint32))
+
+
+def test_forward_1024_experts(gpu):
+    """The largest expert count the scheduler takes (1024): mostly one- to
+    three-row experts, several empty."""
+    d = synth.make_inputs(300, 128, 128, 1024, 8, 38, zipf=None, wdtype="bf16")
+    ref = O.expert_forward(d)
+    say("forward E=1024")
+    dev = to_device(d)
+    r = eaas.alloc_routing(d["T"], d["k"], d["E"])
+    got = forward(dev, d["k"], routing=r).cpu().numpy()
+    assert_routing_equal({key: v.cpu().numpy() for key, v in r.items()}, ref["routing"],
+                         d["T"] * d["k"], d["E"])
+    check_close(got, ref["out"], "E=1024")
+
+
 def test_fp8_path_matches_bf16_on_representable_weights(gpu):
     d8 = synth.make_inputs(300, 512, 256, 4, 2, 35, wdtype="fp8")
     wgu, wdn = O.weights_f32(d8)
