@@ -1232,20 +1232,12 @@ hipError_t launch_pp(const GemmParams& p, int R, int E, hipStream_t stream) {
 // Both operands are e4m3fn with fp32 scales: the weights one per 128x128
 // block, the activations one per row and 128 channels.  A K tile is 128
 // channels, exactly one scale block of both, and 128 bytes per LDS row as in
-// the bf16 loops (same DMA geometry and swizzle).  The block-scaled MFMA
-// (v_mfma_scale_f32_32x32x64_f8f6f4, unit block scales) takes 32 bytes of K
-// per lane; A and B fragments hold the same K bytes in the same order, so the
-// two MFMAs of a 32x32 block per K tile give that tile's dot products in
-// `part`, and acc += (row scale * weight block scale) * part.  (The MFMA's
-// internal sums are narrower than fp32; promoting every 128 channels keeps
-// their error to one K tile's worth.)
-//
-// Tile 128x256, 8 waves of 64x64 in two groups of four (group g: rows
-// 64g..64g+63, all 256 columns).  As in the bf16 ping-pong kernel, the groups
-// alternate, phase by phase, between M (fragment reads of a K tile and the
-// DMA share of the group) and C (the tile's 8 MFMAs, with the promotion of
-// the previous tile's partial sums beside them), so each SIMD's matrix pipe
-// is fed by one of its two waves while the other reads:
+// the bf16 loops (same DMA geometry and swizzle).  (The MFMA's internal sums
+// are narrower than fp32; promoting every 128 channels keeps their error to
+// one K tile's worth.)  As in the bf16 ping-pong kernel, the two groups of
+// four waves alternate, phase by phase, between M (fragment reads of a K
+// tile, its scales and the group's DMA share) and C (the tile's MFMAs with
+// their promotions):
 //   group 0, phase 2t:   M(t): DMA of A tile t+1 (t >= 1, with its row
 //                        scales), fragments and scales of tile t
 //   group 0, phase 2t+1: C(t), then wait until A tile t+1 has landed
@@ -1255,19 +1247,6 @@ hipError_t launch_pp(const GemmParams& p, int R, int E, hipStream_t stream) {
 // A has 2 LDS stages and B 3; a stage is refilled only after both groups have
 // read it.  The gate/up epilogue quantizes h per row over the tile's 128 h
 // columns (the 4 waves of a group combine their row maxima in LDS).
-namespace w8 {
-constexpr int BM = 128, BN = 256, NT = 512, WN = 4, MBW = 2, NBW = 2;
-constexpr int RB = 128;  // bytes per LDS row: 128 fp8 channels
-constexpr int SA = 2, SB = 3;
-constexpr int A_BYTES = BM * RB, AS_BYTES = BM * 4, B_BYTES = BN * RB;
-constexpr int AS_BASE = SA * A_BYTES;
-constexpr int B_BASE = AS_BASE + SA * AS_BYTES;
-constexpr int RED_BASE = B_BASE + SB * B_BYTES;  // gate/up epilogue: row maxima per column wave
-constexpr int LDS_BYTES = RED_BASE + BM * WN * 4;
-constexpr int A_INST = 4;  // 16-byte-per-lane DMAs of a group-0 wave per K tile (+1 of scales)
-constexpr int B_INST = 8;  // of a group-1 wave
-}  // namespace w8
-
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 
 // One wave-wide 4-byte-per-lane DMA (row scales): lane l's 4 bytes at
@@ -1277,13 +1256,49 @@ __device__ __forceinline__ void dma4(const void* base, uint32_t voff, uint32_t l
                :: "v"(voff), "s"(wave_uniform(base)), "s"(lds) : "memory");
 }
 
-template <int KIND>
+// fp8 x fp8 on 16x16x128 block-scaled MFMAs.  One MFMA covers
+// a whole 128-channel K tile (one scale block of both operands), so each
+// 16x16 block's partial sum lives for a few instructions only and is
+// promoted right after its MFMA: acc += (row scale x weight block scale) *
+// part.  Without a second accumulator set a wave can hold 96x64 (6 x 4
+// blocks of 16x16; token block i, weight block j): it reads 20 KiB of
+// fragments per K tile for 24 MFMAs, where a 64x64 wave of 32x32 blocks
+// reads 16 KiB for 16.  Lane l supplies row l%16 and K bytes 32*(l/16) .. +32
+// of each operand; the result block holds token l%16 and weight columns
+// 4*(l/16) .. +3 in lane l.  Tile BM x 256 with BM = 32*MB, 8 waves in two
+// groups (token rows 0 .. BM/2-1 and the rest) that alternate M and C
+// phases as in the bf16 ping-pong.
+// MB = 6 (192-row tiles) for prefill-sized batches, MB = 4 (128 rows) for
+// decode-sized ones; the per-block arithmetic is the same, so the two give
+// bitwise equal results.
+template <int MB>
+struct W8Tile {
+  static constexpr int BM = 32 * MB, BN = 256, NT = 512, WN = 4, NB = 4;
+  static constexpr int RB = 128;
+  static constexpr int SA = 2, SB = 3;
+  static constexpr int A_BYTES = BM * RB, AS_BYTES = BM * 4, B_BYTES = BN * RB;
+  static constexpr int AS_BASE = SA * A_BYTES;
+  static constexpr int B_BASE = AS_BASE + SA * AS_BYTES;
+  static constexpr int RED_BASE = B_BASE + SB * B_BYTES;
+  static constexpr int LDS_BYTES = RED_BASE + BM * WN * 4;
+  static constexpr int A_INST = BM / 32;  // 16-byte DMAs of a group-0 wave per K tile (+1 of scales)
+  static constexpr int B_INST = 8;        // of a group-1 wave
+  static constexpr int AS_CHUNKS = BM / 64;  // 64-row chunks of row scales
+};
+
+template <int KIND, int MB>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void grouped_gemm_w8a8_kernel(GemmParams p) {
-  using namespace w8;
+  using T8 = W8Tile<MB>;
+  constexpr int BM = T8::BM, BN = T8::BN, NT = T8::NT, WN = T8::WN, NB = T8::NB, RB = T8::RB;
+  constexpr int SA = T8::SA, SB = T8::SB, A_BYTES = T8::A_BYTES, AS_BYTES = T8::AS_BYTES;
+  constexpr int B_BYTES = T8::B_BYTES, AS_BASE = T8::AS_BASE, B_BASE = T8::B_BASE;
+  constexpr int RED_BASE = T8::RED_BASE, LDS_BYTES = T8::LDS_BYTES;
+  constexpr int A_INST = T8::A_INST, B_INST = T8::B_INST;
   constexpr bool GATEUP = KIND == kGateUp;
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
-  static_assert(AS_BASE >= (2 * kMaxExperts + 2 + NT / kWave) * 4, "scheduler tables");
+  static_assert(AS_BASE >= (2 * kMaxExperts + 2 + 2 * (NT / kWave)) * 4, "scheduler tables");
+  static_assert(A_INST * 4 * 8 == BM && B_INST * 4 * 8 == BN, "DMA rows");
   __shared__ __attribute__((aligned(1024))) char smem_raw[LDS_BYTES];
 
   Tile t;
@@ -1297,23 +1312,23 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
-  const int grp = wave >> 2;  // 0: rows 0-63, streams A; 1: rows 64-127, streams B
+  const int grp = wave >> 2;  // 0: rows 0 .. BM/2-1, streams A; 1: the rest, streams B
   const int wn = wave & 3;
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem_raw);
-  const int nk = p.K / 128;  // K tiles = scale blocks along K
+  const int nk = p.K / 128;
 
-  // DMA: instruction q of wave wn of a group moves rows (wn + 4q)*8 .. +8 of
-  // the group's operand; lane l writes 16 bytes at (row l/8, physical chunk
-  // l%8), so it fetches logical chunk (l%8) ^ swizzle(row).  Group 0's scale
-  // DMA from wave wn covers rows (wn%2)*64 .. +64 (two waves write each half,
-  // the same bytes).
   auto src_row = [&](int row) {
     const int r = t.r0 + (row < t.rows_valid ? row : 0);
     return GATEUP ? min(max(p.perm[r], 0), p.R - 1) / p.k : r;
   };
+  // DMA: instruction q of wave wn moves rows (wn + 4q)*8 .. +8 of the group's
+  // operand (lane l: row l/8, physical chunk l%8, logical chunk (l%8) ^
+  // swizzle(row)).  Row scales: wave wn writes rows min(wn, chunks-1)*64 .. +64
+  // (the last chunk's bytes written twice over, so every wave issues one).
   const char* dbase;
   uint32_t doff[B_INST];
   uint32_t asoff = 0;
+  const int as_chunk = min(wn, T8::AS_CHUNKS - 1);
   {
     const int drow = lane >> 3, dpc = lane & 7;
     if (grp == 0) {
@@ -1323,7 +1338,7 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
         const int row = (wn + 4 * (q % A_INST)) * 8 + drow;
         doff[q] = (uint32_t)src_row(row) * (uint32_t)p.K + (uint32_t)((dpc ^ swz<RB>(row)) * 16);
       }
-      asoff = (uint32_t)src_row((wn & 1) * 64 + lane) * (uint32_t)nk * 4u;
+      asoff = (uint32_t)src_row(as_chunk * 64 + lane) * (uint32_t)nk * 4u;
     } else {
       dbase = reinterpret_cast<const char*>(group_weights(p, t.e, 1));
 #pragma unroll
@@ -1335,13 +1350,12 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
     }
   }
   const char* asbase = reinterpret_cast<const char*>(p.a_scale);
-  // DMA of K tile kt of this group's operand into its ring slot
   auto issue = [&](int kt) {
     if (grp == 0) {
       const uint32_t dst = lds0 + (kt % SA) * A_BYTES + wn * 8 * RB;
 #pragma unroll
       for (int q = 0; q < A_INST; ++q) dma16(dbase + kt * RB, doff[q], dst + q * 4 * 8 * RB);
-      dma4(asbase + kt * 4, asoff, lds0 + AS_BASE + (kt % SA) * AS_BYTES + (wn & 1) * 256);
+      dma4(asbase + kt * 4, asoff, lds0 + AS_BASE + (kt % SA) * AS_BYTES + as_chunk * 256);
     } else {
       const uint32_t dst = lds0 + B_BASE + (kt % SB) * B_BYTES + wn * 8 * RB;
 #pragma unroll
@@ -1349,175 +1363,157 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
     }
   };
 
-  const int lrow = lane & 31;
-  const int khalf = lane >> 5;
-  const int am0 = grp * MBW * 32;
-  const int a_lane_off = (am0 + lrow) * RB;
-  int b_lane_off[NBW];
-  const CONST_AS float* sc[NBW];  // per N block: its row of weight block scales
+  const int l16 = lane & 15;
+  const int kq = lane >> 4;
+  const int am0 = grp * (MB * 16);
+  const int a_lane_off = (am0 + l16) * RB;
+  int b_lane_off[NB];
+  const CONST_AS float* sc[NB];  // per weight block: its row of 128x128 scales
 #pragma unroll
-  for (int j = 0; j < NBW; ++j) {
-    const int br = block_row<GATEUP, BN, NBW>(wn, j);
-    b_lane_off[j] = (br + lrow) * RB;
+  for (int j = 0; j < NB; ++j) {
+    const int br = GATEUP ? (j < 2 ? wn * 32 + 16 * j : BN / 2 + wn * 32 + 16 * (j - 2))
+                          : wn * 64 + 16 * j;
+    b_lane_off[j] = (br + l16) * RB;
     sc[j] = (const CONST_AS float*)wave_uniform(
         group_scales(p, t.e) + (size_t)(weight_row<GATEUP, BN>(p, t.tn, br) / 128) * nk);
   }
-  const int s_l = swz<RB>(lrow);  // rows am0 + 32i + lrow share lrow's swizzle
+  const int s_l = swz<RB>(l16);  // rows am0 + 16i + l16 share l16's swizzle
   const int mb_live =
-      __builtin_amdgcn_readfirstlane(max(0, min(MBW, ceil_div(t.rows_valid - am0, 32))));
+      __builtin_amdgcn_readfirstlane(max(0, min(MB, ceil_div(t.rows_valid - am0, 16))));
   const LDS_AS char* smem = (const LDS_AS char*)smem_raw;
 
-  // the 32 bytes of K step kk (0, 1) of the row at lane_off, for this lane
-  auto frag = [&](const LDS_AS char* base, int lane_off, int kk) {
-    const int c0 = kk * 4 + khalf * 2;
+  // this lane's 32 bytes (chunks 2kq, 2kq+1) of the row at lane_off
+  auto frag = [&](const LDS_AS char* base, int lane_off) {
+    const int c0 = 2 * kq;
     const u32x4 lo = *reinterpret_cast<const LDS_AS u32x4*>(base + lane_off + ((c0 ^ s_l) << 4));
     const u32x4 hi =
         *reinterpret_cast<const LDS_AS u32x4*>(base + lane_off + (((c0 + 1) ^ s_l) << 4));
     return i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
                  (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
   };
-  auto mma = [&](const i32x8& b, const i32x8& a, const f32x16& c) {
-    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b, a, c, 0, 0, 0, 127, 0, 127);
-  };
 
-  f32x16 acc[MBW][NBW], part[MBW][NBW];
+  f32x4 acc[MB][NB];
 #pragma unroll
-  for (int i = 0; i < MBW; ++i)
+  for (int i = 0; i < MB; ++i)
 #pragma unroll
-    for (int j = 0; j < NBW; ++j) {
-      acc[i][j] = f32x16{};
-      part[i][j] = f32x16{};
-    }
-  i32x8 fa[2][MBW], fb[2][NBW];
-  // scale products (row scale x weight block scale): f of the tile in
-  // `part` (0 before the first), fn of the tile whose fragments are loaded
-  float f[MBW][NBW], fn[MBW][NBW];
-#pragma unroll
-  for (int i = 0; i < MBW; ++i)
-#pragma unroll
-    for (int j = 0; j < NBW; ++j) f[i][j] = fn[i][j] = 0.0f;
+    for (int j = 0; j < NB; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
   auto phase_end = [&]() {
-    // keep the scheduler from moving MFMAs or LDS reads across the barrier
     __builtin_amdgcn_sched_barrier(0);
     lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
-  // M(kt): fragments and scales of tile kt; promotion of the previous tile
-  auto load_tile = [&](int kt) {
-    const LDS_AS char* as = smem + (kt % SA) * A_BYTES;
-    const LDS_AS char* bs = smem + B_BASE + (kt % SB) * B_BYTES;
+  auto main_loop = [&](auto full) {
+    constexpr bool FULL = decltype(full)::value;
+    i32x8 fa[MB], fb[NB];
+    float rsc[MB], wsc[NB];
+    // M(kt): the tile's fragments and scales
+    auto load_tile = [&](int kt) {
+      const LDS_AS char* as = smem + (kt % SA) * A_BYTES;
+      const LDS_AS char* bs = smem + B_BASE + (kt % SB) * B_BYTES;
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
+      for (int j = 0; j < NB; ++j) fb[j] = frag(bs, b_lane_off[j]);
 #pragma unroll
-      for (int j = 0; j < NBW; ++j) fb[kk][j] = frag(bs, b_lane_off[j], kk);
+      for (int i = 0; i < MB; ++i)
+        if (FULL || i < mb_live) fa[i] = frag(as, a_lane_off + i * 16 * RB);
 #pragma unroll
-      for (int i = 0; i < MBW; ++i) fa[kk][i] = frag(as, a_lane_off + i * 32 * RB, kk);
-    }
-    float wsc[NBW], rsc[MBW];
+      for (int j = 0; j < NB; ++j) wsc[j] = sc[j][kt];
 #pragma unroll
-    for (int j = 0; j < NBW; ++j) wsc[j] = sc[j][kt];
+      for (int i = 0; i < MB; ++i)
+        if (FULL || i < mb_live)
+          rsc[i] = *reinterpret_cast<const LDS_AS float*>(smem + AS_BASE + (kt % SA) * AS_BYTES +
+                                                          (am0 + i * 16 + l16) * 4);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    };
+    // C(kt): one MFMA per block, each promoted two blocks later (the
+    // VALU work runs beside the matrix pipe)
+    auto mfmas = [&]() {
+      __builtin_amdgcn_s_setprio(1);
+      f32x4 pr[3];
+      constexpr int NBLK = MB * NB;
 #pragma unroll
-    for (int i = 0; i < MBW; ++i)
-      rsc[i] = *reinterpret_cast<const LDS_AS float*>(smem + AS_BASE + (kt % SA) * AS_BYTES +
-                                                      (am0 + i * 32 + lrow) * 4);
+      for (int b = 0; b < NBLK + 2; ++b) {
+        if (b < NBLK) {
+          const int i = b / NB, j = b % NB;
+          if (FULL || i < mb_live)
+            pr[b % 3] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
+                fb[j], fa[i], f32x4{0.0f, 0.0f, 0.0f, 0.0f}, 0, 0, 0, 127, 0, 127);
+        }
+        if (b >= 2) {
+          const int c = b - 2, i = c / NB, j = c % NB;
+          if (FULL || i < mb_live) {
+            const float f = rsc[i] * wsc[j];
 #pragma unroll
-    for (int i = 0; i < MBW; ++i)
-#pragma unroll
-      for (int j = 0; j < NBW; ++j) fn[i][j] = rsc[i] * wsc[j];
-    // the stage may be refilled right after the next barrier
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  };
-  // C(kt): the tile's MFMAs into `part`; before each block's first MFMA, the
-  // previous tile's partial sums of that block are promoted (VALU work that
-  // runs beside the matrix pipe)
-  // the C phase runs at raised wave priority, as in the bf16 ping-pong
-  auto mfmas = [&]() {
-    __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-    for (int i = 0; i < MBW; ++i)
-#pragma unroll
-      for (int j = 0; j < NBW; ++j) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[i][j][v] += f[i][j] * part[i][j][v];
-        f[i][j] = fn[i][j];
-        part[i][j] = mma(fb[0][j], fa[0][i], f32x16{});
+            for (int v = 0; v < 4; ++v) acc[i][j][v] += f * pr[c % 3][v];
+          }
+        }
       }
-#pragma unroll
-    for (int i = 0; i < MBW; ++i)
-#pragma unroll
-      for (int j = 0; j < NBW; ++j) part[i][j] = mma(fb[1][j], fa[1][i], part[i][j]);
-    __builtin_amdgcn_s_setprio(0);
+      __builtin_amdgcn_s_setprio(0);
+    };
+
+    constexpr int INST_G0 = A_INST + 1;
+    issue(0);
+    if (nk > 1) {
+      issue(1);
+      if (grp == 0) wait_vmcnt<INST_G0>();
+      else wait_vmcnt<B_INST>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    phase_end();
+    if (grp == 0) {
+      for (int kt = 0; kt < nk; ++kt) {
+        if (kt >= 1 && kt + 1 < nk) issue(kt + 1);
+        load_tile(kt);
+        phase_end();
+        mfmas();
+        wait_vmcnt<0>();  // A tile kt+1 (issued in the previous phase) has landed
+        phase_end();
+      }
+      phase_end();
+    } else {
+      phase_end();
+      for (int kt = 0; kt < nk; ++kt) {
+        if (kt + 2 < nk) issue(kt + 2);
+        load_tile(kt);
+        if (kt + 2 < nk) wait_vmcnt<B_INST>();
+        else wait_vmcnt<0>();
+        phase_end();
+        mfmas();
+        phase_end();
+      }
+    }
   };
+  if (t.rows_valid == BM) main_loop(std::true_type{});
+  else main_loop(std::false_type{});
 
-  // prologue: each group's first two K tiles of its operand; tile 0 must
-  // have landed before the first barrier
-  constexpr int INST_G0 = A_INST + 1;
-  issue(0);
-  if (nk > 1) {
-    issue(1);
-    if (grp == 0) wait_vmcnt<INST_G0>();
-    else wait_vmcnt<B_INST>();
-  } else {
-    wait_vmcnt<0>();
-  }
-  phase_end();
-  // both groups pass 2*nk + 1 phase barriers: group 1 idles in the first
-  // phase, group 0 in the last
-  if (grp == 0) {
-    for (int kt = 0; kt < nk; ++kt) {
-      if (kt >= 1 && kt + 1 < nk) issue(kt + 1);
-      load_tile(kt);
-      phase_end();
-      mfmas();
-      wait_vmcnt<0>();  // A tile kt+1 (issued in the previous phase) has landed
-      phase_end();
-    }
-    phase_end();
-  } else {
-    phase_end();
-    for (int kt = 0; kt < nk; ++kt) {
-      if (kt + 2 < nk) issue(kt + 2);
-      load_tile(kt);
-      // B tile kt+1 has landed; B tile kt+2 may still be in flight
-      if (kt + 2 < nk) wait_vmcnt<B_INST>();
-      else wait_vmcnt<0>();
-      phase_end();
-      mfmas();
-      phase_end();
-    }
-  }
-  // promotion of the last tile
-#pragma unroll
-  for (int i = 0; i < MBW; ++i)
-#pragma unroll
-    for (int j = 0; j < NBW; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] += f[i][j] * part[i][j][v];
-
+  // acc[i][j][v]: token row am0 + 16i + l16, weight column 4*kq + v of block j
   if constexpr (GATEUP) {
-    // h = bf16(silu(g) * u), then per row over the tile's 128 h columns:
-    // s = amax / 448, q = e4m3(h / s).  This wave holds 32 of the columns
-    // (gate block j = 0 paired with up block j = 1), half in each lane half.
+    // h = bf16(silu(g) * u); per row over the tile's 128 h columns:
+    // s = amax / 448, q = e4m3(h / s).  This wave holds 32 of them (gate
+    // blocks 0, 1 paired with up blocks 2, 3), 4 per lane per block.
     float* red = reinterpret_cast<float*>(smem_raw + RED_BASE);  // [BM][WN]
-    float hv[MBW][16];
+    float hv[MB][2][4];
 #pragma unroll
-    for (int i = 0; i < MBW; ++i) {
+    for (int i = 0; i < MB; ++i) {
       float m = 0.0f;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float h = silu_mul(acc[i][0][v], acc[i][1][v]);
-        hv[i][v] = __uint_as_float(f32_to_bf16_bits(h) << 16);
-        m = fmaxf(m, fabsf(hv[i][v]));
-      }
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float h = silu_mul(acc[i][j][v], acc[i][j + 2][v]);
+          hv[i][j][v] = __uint_as_float(f32_to_bf16_bits(h) << 16);
+          m = fmaxf(m, fabsf(hv[i][j][v]));
+        }
+      m = fmaxf(m, __shfl_xor(m, 16));
       m = fmaxf(m, __shfl_xor(m, 32));
-      if (khalf == 0) red[(am0 + i * 32 + lrow) * WN + wn] = m;
+      if (kq == 0) red[(am0 + i * 16 + l16) * WN + wn] = m;
     }
     __syncthreads();
-    const int nkh = p.I / 128;  // h scale blocks per row
+    const int nkh = p.I / 128;
 #pragma unroll
-    for (int i = 0; i < MBW; ++i) {
-      const int rr = am0 + i * 32 + lrow;
+    for (int i = 0; i < MB; ++i) {
+      const int rr = am0 + i * 16 + l16;
       if (rr >= t.rows_valid) continue;
       const int r = t.r0 + rr;
       float m = 0.0f;
@@ -1526,31 +1522,80 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
       const float s = m > 0.0f ? m / 448.0f : 1.0f;
       uint8_t* qrow = p.hq + (size_t)r * p.I + t.tn * (BN / 2) + wn * 32;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int c = 8 * g + 4 * khalf;
-        *reinterpret_cast<uint32_t*>(qrow + c) =
-            pack_e4m3x4(hv[i][4 * g] / s, hv[i][4 * g + 1] / s, hv[i][4 * g + 2] / s,
-                        hv[i][4 * g + 3] / s);
-      }
-      if (wn == 0 && khalf == 0) p.hs[(size_t)r * nkh + t.tn] = s;
+      for (int j = 0; j < 2; ++j)
+        *reinterpret_cast<uint32_t*>(qrow + 16 * j + 4 * kq) =
+            pack_e4m3x4(hv[i][j][0] / s, hv[i][j][1] / s, hv[i][j][2] / s, hv[i][j][3] / s);
+      if (wn == 0 && kq == 0) p.hs[(size_t)r * nkh + t.tn] = s;
     }
   } else {
-    // after the loop's last barrier: no wave reads the stages any more
-    const RowInfo<MBW> ri = row_info<KIND, MBW>(p, t, am0, mb_live);
-    static_assert(8 * kRowsLdsBytes<NBW> <= LDS_BYTES, "epilogue regions");
-    epilogue_rows_lds<KIND, BN, MBW, NBW>(
-        p, t, wn, am0, mb_live, ri, acc, (LDS_AS float*)(smem_raw + wave * kRowsLdsBytes<NBW>));
+    // after the loop's last barrier no wave reads the stages: each wave
+    // stages 32 rows (two token blocks) at a time in its own LDS region and
+    // stores whole 256-byte row segments
+    int orow[MB];
+    float wt[MB];
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+      const int rr = am0 + i * 16 + l16;
+      const int r = t.r0 + (rr < t.rows_valid ? rr : 0);
+      orow[i] = r;
+      wt[i] = 1.0f;
+      if (KIND == kDownWeightedK && i < mb_live) {
+        orow[i] = min(max(p.perm[r], 0), p.R - 1);
+        wt[i] = p.w[orow[i]];
+      }
+    }
+    constexpr int COLS = NB * 16, LD = COLS + 4, LPR = COLS / 4, RPI = kWave / LPR;
+    static_assert(8 * 32 * LD * 4 <= LDS_BYTES, "epilogue regions");
+    LDS_AS float* buf = (LDS_AS float*)(smem_raw + wave * (32 * LD * 4));
+    const int rl = lane / LPR, cl = (lane % LPR) * 4;
+    float* ybase = p.y + t.tn * BN + wn * COLS + cl;
+#pragma unroll
+    for (int pb = 0; pb < MB / 2; ++pb) {
+      if (2 * pb >= mb_live) break;
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int i = 2 * pb + h2;
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          f32x4 v;
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            v[u] = KIND == kDownWeightedK ? wt[i] * acc[i][j][u] : acc[i][j][u];
+          *reinterpret_cast<LDS_AS f32x4*>(buf + (16 * h2 + l16) * LD + 16 * j + 4 * kq) = v;
+        }
+      }
+#pragma unroll
+      for (int sidx = 0; sidx < 32 / RPI; ++sidx) {
+        const int m = sidx * RPI + rl;
+        const f32x4 v = *reinterpret_cast<const LDS_AS f32x4*>(buf + m * LD + cl);
+        const int o0 = __shfl(orow[2 * pb], m & 15);
+        const int o1 = __shfl(orow[2 * pb + 1], m & 15);
+        const int o = m < 16 ? o0 : o1;
+        if (am0 + pb * 32 + m < t.rows_valid)
+          __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(ybase + (size_t)o * p.N));
+      }
+    }
   }
 }
 
-template <int KIND>
-hipError_t launch_w8a8(const GemmParams& p, int R, int E, hipStream_t stream) {
-  const long long grid = grid_tiles(R, E, w8::BM, w8::BN, p.N);
+template <int KIND, int MB>
+hipError_t launch_w8a8_mb(const GemmParams& p, int R, int E, hipStream_t stream) {
+  using T8 = W8Tile<MB>;
+  const long long grid = grid_tiles(R, E, T8::BM, T8::BN, p.N);
   if (grid <= 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((grouped_gemm_w8a8_kernel<KIND>), dim3((unsigned)grid), dim3(w8::NT), 0,
+  hipLaunchKernelGGL((grouped_gemm_w8a8_kernel<KIND, MB>), dim3((unsigned)grid), dim3(T8::NT), 0,
                      stream, p);
   return hipGetLastError();
+}
+
+// 192-row tiles for prefill-sized batches; 128-row tiles when an expert gets
+// about one 128-row tile or less (decode), where taller tiles would only
+// stream more empty token rows.  Both give the same bits.
+template <int KIND>
+hipError_t launch_w8a8(const GemmParams& p, int R, int E, bool small_m, hipStream_t stream) {
+  return small_m ? launch_w8a8_mb<KIND, 4>(p, R, E, stream)
+                 : launch_w8a8_mb<KIND, 6>(p, R, E, stream);
 }
 
 // Tile shapes (N a multiple of 256 takes the LDS-DMA kernels):
@@ -1624,7 +1669,7 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
     g.a_scale = a.xs;
     g.hq = a.hq;
     g.hs = a.hs;
-    return launch_w8a8<kGateUp>(g, R, a.E, stream);
+    return launch_w8a8<kGateUp>(g, R, a.E, small_rows(a), stream);
   }
   return a.fp8 ? launch_kind<kGateUp, true>(g, R, a.E, small_rows(a), stream)
                : launch_kind<kGateUp, false>(g, R, a.E, small_rows(a), stream);
@@ -1645,8 +1690,8 @@ hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
   if (a.act8) {
     g.a8 = a.hq;
     g.a_scale = a.hs;
-    return a.epilogue == kDownWeighted ? launch_w8a8<kDownWeightedK>(g, R, a.E, stream)
-                                       : launch_w8a8<kDownPlainK>(g, R, a.E, stream);
+    return a.epilogue == kDownWeighted ? launch_w8a8<kDownWeightedK>(g, R, a.E, small_rows(a), stream)
+                                       : launch_w8a8<kDownPlainK>(g, R, a.E, small_rows(a), stream);
   }
   const bool sm = small_rows(a);
   if (a.epilogue == kDownWeighted)
