@@ -28,8 +28,12 @@
 //     sum is scaled and added to the fp32 accumulator
 //     (grouped_gemm_dma_kernel);
 //   - fp8 weights with fp8 activations (one fp32 scale per row and 128
-//     channels): a ping-pong on block-scaled fp8 MFMAs, promoting every K
-//     tile (grouped_gemm_w8a8_kernel).
+//     channels): a ping-pong on 16x16x128 block-scaled fp8 MFMAs, each
+//     block's partial sum promoted after its K tile (grouped_gemm_w8a8_kernel).
+// In the ping-pong loops the multiplying group runs at raised wave priority.
+// The fp8-weight down projection runs two 4-wave workgroups per CU.  The
+// down epilogues stage each wave's accumulators through LDS so the fp32
+// rows go out as whole 256-byte row segments.
 // A register-staged loop covers shapes the DMA tiles do not (N not a multiple
 // of 256).
 // LDS rows are BK elements long; 16-byte chunk c of row r is stored at chunk
@@ -1599,13 +1603,16 @@ hipError_t launch_w8a8(const GemmParams& p, int R, int E, bool small_m, hipStrea
 }
 
 // Tile shapes (N a multiple of 256 takes the LDS-DMA kernels):
-//   bf16, prefill-sized: 256x256 tiles, 8 waves of 128x64 in ping-pong, BK=64;
-//   fp8 weights: 96x512 tiles (a decode batch's ~50-90 rows per expert fit
-//     one tile, so the weights stream once), 8 waves of 96x64 -- two per
-//     SIMD, so one wave's partial-sum scaling (VALU) overlaps the other's
-//     MFMAs -- BK=64, 2 token-row stages and 4 weight stages (152 KiB), so
-//     96 KiB of weights per CU are in flight while a tile is multiplied
-//     (96x256 with 4 waves and 3+3 stages when N is not a multiple of 512);
+//   bf16: 256x256 tiles, 8 waves of 128x64 in ping-pong, BK=64;
+//   fp8 weights, gate/up: 96x512 tiles (a decode batch's ~50-90 rows per
+//     expert fit one tile, so the weights stream once), 8 waves of 96x64 --
+//     two per SIMD, so one wave's partial-sum scaling (VALU) overlaps the
+//     other's MFMAs -- BK=64, 2 token-row stages and 4 weight stages
+//     (152 KiB), so 96 KiB of weights per CU are in flight while a tile is
+//     multiplied (96x256 with 4 waves and 3+3 stages when N is not a
+//     multiple of 512);
+//   fp8 weights, down: 96x256 tiles of 4 waves, two workgroups per CU;
+//   fp8 weights and activations: 192x256 (prefill) or 128x256 (decode);
 //   N not a multiple of 256: register-staged 128-row tiles.
 template <int KIND, bool FP8>
 hipError_t launch_kind(const GemmParams& p, int R, int E, bool small_m, hipStream_t stream) {
