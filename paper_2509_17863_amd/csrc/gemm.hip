@@ -1550,6 +1550,7 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
     }
     constexpr int COLS = NB * 16, LD = COLS + 4, LPR = COLS / 4, RPI = kWave / LPR;
     static_assert(8 * 32 * LD * 4 <= LDS_BYTES, "epilogue regions");
+    static_assert(MB % 2 == 0, "the passes below take token blocks in pairs");
     LDS_AS float* buf = (LDS_AS float*)(smem_raw + wave * (32 * LD * 4));
     const int rl = lane / LPR, cl = (lane % LPR) * 4;
     float* ybase = p.y + t.tn * BN + wn * COLS + cl;
