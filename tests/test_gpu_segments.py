@@ -155,6 +155,20 @@ def test_segments_fp8_activations(gpu):
     check_against(reqs, bufs, forward_concat(d, reqs, act8=True))
 
 
+def test_fp8_activation_tile_heights_agree(gpu):
+    """The fp8 x fp8 GEMMs take 128-row tiles when T*k <= 128*E and 192-row
+    tiles above.  Here the concatenated batch (about 240 tokens, T*k <= 2048)
+    takes the short tiles and the segmented step sized for 1024 tokens the
+    tall ones; the per-block arithmetic is the same, so the bits agree."""
+    rng = np.random.default_rng(12)
+    sizes = [int(v) for v in rng.integers(0, 40, size=12)]
+    d, reqs = make_requests(sizes, H=512, I=256, E=16, k=4, seed=45, wdtype="fp8")
+    assert sum(sizes) * 4 <= 128 * 16 < 1024 * 4
+    say("fp8 activations, 128- and 192-row tiles", sum(sizes))
+    bufs, _ = run_segments(d, reqs, 1024, act8=True)
+    check_against(reqs, bufs, forward_concat(d, reqs, act8=True))
+
+
 def test_segments_capacity_cuts_the_batch(gpu):
     d, reqs = make_requests([50, 80, 40])
     say("segments capacity 100 of 170")
