@@ -87,9 +87,43 @@ def measured_traffic(workload: str):
     return int(rec["traffic_bytes"])
 
 
-def cpu_baseline(d: dict, target_s: float = 12.0) -> dict:
-    """The oracle, untuned, on a bounded token sample (weights pre-converted
-    to fp64 outside the timed region)."""
+def host_info() -> dict:
+    """CPU model of the host and the BLAS NumPy calls (the oracle's matmuls)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
+    try:
+        b = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        blas = f"{b.get('name')} {b.get('version')}"
+        conf = b.get("openblas configuration")
+        if conf:
+            blas += f" ({conf})"
+    except Exception:  # noqa: BLE001 - metadata only
+        pass
+    return {"cpu_model": model, "blas": blas, "numpy": np.__version__}
+
+
+def _median_runs(run, T: int, target_s: float, repeats: int = 3):
+    """Calibrate a token count so one run takes about target_s, then time
+    `repeats` runs on fresh samples of that size; the median rate."""
+    n = min(T, 64)
+    t = run(n)
+    if t < target_s and n < T:
+        n = int(min(T, max(n, n * target_s / max(t, 1e-3))))
+    times = [run(n) for _ in range(repeats)]
+    return n, times
+
+
+def cpu_baseline(d: dict, target_s: float = 5.0) -> dict:
+    """The oracle, untuned, on bounded token samples of the same batch
+    (weights pre-converted to fp64 outside the timed region); median of 3."""
     from oracle import eaas_oracle as O
 
     if d.get("act8"):
@@ -110,19 +144,21 @@ def cpu_baseline(d: dict, target_s: float = 12.0) -> dict:
         O.expert_forward(sub, weights=w64)
         return time.perf_counter() - t0
 
-    n = min(d["T"], 64)
-    t = run(n)
-    if t < target_s and n < d["T"]:
-        n = int(min(d["T"], max(n, n * target_s / max(t, 1e-3))))
-        t = run(n)
-    return {"value": n / t, "unit": "tokens/s", "cores": cpu_threads(), "kind": "oracle",
-            "sample": f"{n} of {d['T']} tokens of the same batch (oracle expert_forward on the "
-                      f"sub-batch, fp64 BLAS, {t:.1f} s; weights converted to fp64 beforehand)"}
+    n, times = _median_runs(run, d["T"], target_s)
+    t = float(np.median(times))
+    flops = 6.0 * n * d["k"] * d["H"] * d["I"]
+    return {"value": round(n / t, 1), "unit": "tokens/s", "cores": cpu_threads(), "kind": "oracle",
+            "gflops": round(flops / t / 1e9, 1), "runs_s": [round(x, 2) for x in times],
+            **host_info(),
+            "sample": f"{n} of {d['T']} tokens of the same batch, median of {len(times)} runs "
+                      f"on fresh samples (oracle expert_forward on the sub-batch, fp64 BLAS; "
+                      "weights converted to fp64 beforehand)"}
 
 
-def cpu_baseline_w8a8(d: dict, target_s: float = 12.0) -> dict:
-    """The fp8-activation oracle, untuned, on a bounded token sample (it
-    dequantizes each active expert's weights inside the timed region)."""
+def cpu_baseline_w8a8(d: dict, target_s: float = 5.0) -> dict:
+    """The fp8-activation oracle, untuned, on bounded token samples (it
+    dequantizes each active expert's weights inside the timed region);
+    median of 3."""
     from oracle import eaas_oracle as O
     from oracle import w8a8_oracle as W
 
@@ -135,15 +171,13 @@ def cpu_baseline_w8a8(d: dict, target_s: float = 12.0) -> dict:
         W.expert_forward_w8a8(sub)
         return time.perf_counter() - t0
 
-    n = min(d["T"], 64)
-    t = run(n)
-    if t < target_s and n < d["T"]:
-        n = int(min(d["T"], max(n, n * target_s / max(t, 1e-3))))
-        t = run(n)
-    return {"value": n / t, "unit": "tokens/s", "cores": cpu_threads(), "kind": "oracle",
-            "sample": f"{n} of {d['T']} tokens of the same batch (fp8-activation oracle on the "
-                      f"sub-batch, fp64 BLAS, {t:.1f} s including the per-expert weight "
-                      "dequantization)"}
+    n, times = _median_runs(run, d["T"], target_s)
+    t = float(np.median(times))
+    return {"value": round(n / t, 1), "unit": "tokens/s", "cores": cpu_threads(), "kind": "oracle",
+            "runs_s": [round(x, 2) for x in times], **host_info(),
+            "sample": f"{n} of {d['T']} tokens of the same batch, median of {len(times)} runs "
+                      "(fp8-activation oracle on the sub-batch, fp64 BLAS, including the "
+                      "per-expert weight dequantization)"}
 
 
 def time_graph(step, steps: int, warmup: int) -> tuple[float, dict]:
@@ -290,12 +324,137 @@ def time_server(d: dict, dev: dict, n_slots: int, steps: int, warmup: int, ms_si
             "vs_single_batch": round(ms / ms_single, 4)}
 
 
+def measure(name: str, steps: int, warmup: int):
+    """Time eaas_expert_forward on one workload: a graph-replayed pass for the
+    step time and an eager pass with events between the kernels."""
+    import torch
+
+    from paper_2509_17863_amd import eaas, synth
+    from paper_2509_17863_amd.device_io import to_device
+
+    wl = synth.WORKLOADS[name]
+    d = synth.make_workload(name)
+    dev = to_device(d)
+    T, H, I, E, k = d["T"], d["H"], d["I"], d["E"], d["k"]
+    act8 = bool(d.get("act8"))
+    wdt = (eaas.EAAS_FP8_E4M3_A8 if act8 else eaas.EAAS_FP8_E4M3) if d["wdtype"] == "fp8" \
+        else eaas.EAAS_BF16
+    ws = eaas.alloc_workspace(T, H, I, E, k, wdt)
+    out = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
+    counts = np.bincount(d["topk_ids"].ravel()[d["topk_ids"].ravel() >= 0], minlength=E)
+    alg = algorithmic(d, counts)
+
+    stream = torch.cuda.current_stream()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+
+    def step(ev=None):
+        if ev is None:
+            eaas.eaas_expert_forward(dev["x"], dev["topk_ids"], dev["topk_weights"],
+                                     dev["w_gate_up"], dev["w_down"], out, ws,
+                                     dev["w_gate_up_scale"], dev["w_down_scale"], act8=act8)
+        else:
+            eaas.eaas_expert_forward_profiled(dev["x"], dev["topk_ids"], dev["topk_weights"],
+                                              dev["w_gate_up"], dev["w_down"], out, ws,
+                                              dev["w_gate_up_scale"], dev["w_down_scale"],
+                                              events=ev, act8=act8)
+
+    for ev in evs:  # create the events before the timed region
+        for e in ev:
+            e.record(stream)
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / steps
+
+    def mean_ms(a, b):
+        return float(np.mean([evs[i][a].elapsed_time(evs[i][b]) for i in range(steps)]))
+
+    # the step as the paper deploys it (§4.3): captured once in a graph, then
+    # replayed; the same kernels with no launches from the host per step
+    ms_graph, graph_stats = time_graph(step, steps, warmup)
+
+    t_route, t_gu, t_dn, t_comb = mean_ms(0, 1), mean_ms(1, 2), mean_ms(2, 3), mean_ms(3, 4)
+    t_step_ev = mean_ms(0, 4)
+    # the gate/up launch's bound: HBM when its algorithmic intensity is below
+    # the ridge of the MFMA peak it runs on (fp8 x fp8 with fp8 activations,
+    # bf16 otherwise), the matrix cores above it
+    peak_flops = PEAK_FP8_TFLOPS if act8 else PEAK_BF16_TFLOPS
+    intensity = alg["gu_flops"] / alg["gu_bytes"]
+    hbm_bound = intensity < peak_flops * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if hbm_bound:
+        achieved = alg["gu_bytes"] / (t_gu * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    else:
+        # a contraction is priced against the MFMA peak of its own dtype
+        achieved = alg["gu_flops"] / (t_gu * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak_flops,
+                "unit": "TFLOP/s", "frac": round(achieved / peak_flops, 4)}
+    roof["traffic"] = measured_traffic(name)
+    roof["traffic_unit"] = "bytes per launch"
+    roof["algorithmic_bytes"] = int(alg["gu_bytes"])
+    roof["algorithmic_flops"] = alg["gu_flops"]
+    roof["launch_ms"] = round(t_gu, 4)
+    roof["kernel"] = gate_up_kernel_name(d)
+    res = {
+        "value": round(T / (ms_graph * 1e-3), 1),
+        "ms_per_step": round(ms_graph, 4),
+        "graph_replay_ms": graph_stats,
+        "eager": {"ms_per_step": round(ms, 4), "value": round(T / (ms * 1e-3), 1),
+                  "graph_speedup": round(ms / ms_graph, 4)},
+        "dtype": "fp8e4m3" if act8 else "bf16",
+        "config": {"workload": name, "T": T, "H": H, "I": I, "E": E, "k": k,
+                   "weights": d["wdtype"], "activations": "fp8e4m3" if act8 else "bf16",
+                   "seed": wl.seed, "zipf": wl.zipf,
+                   "active_experts": int((counts > 0).sum()), "parallelism": "none (1 GPU)"},
+        "step_tflops": round(alg["flops"] / (ms_graph * 1e-3) / 1e12, 1),
+        "step_frac_bf16_peak": round(alg["flops"] / (ms_graph * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        # the two grouped GEMMs alone: 6RHI over their summed event times
+        "gemm_tflops": round(alg["flops"] / ((t_gu + t_dn) * 1e-3) / 1e12, 1),
+        "gemm_frac_bf16_peak": round(alg["flops"] / ((t_gu + t_dn) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "kernels_ms": {"route": round(t_route, 4), "gate_up": round(t_gu, 4),
+                       "down": round(t_dn, 4), "combine": round(t_comb, 4),
+                       "step_events": round(t_step_ev, 4)},
+        "down_tflops": round(alg["dn_flops"] / (t_dn * 1e-3) / 1e12, 1),
+        "roofline": roof,
+    }
+    if hbm_bound:
+        # the weight-streaming regime: algorithmic bytes of both GEMMs over
+        # the whole replayed step, and the gate/up launch alone
+        step_gbs = (alg["gu_bytes"] + alg["dn_bytes"]) / (ms_graph * 1e-3) / 1e9
+        res["step_hbm_gbs"] = round(step_gbs, 1)
+        res["step_hbm_frac"] = round(step_gbs / PEAK_HBM_GBS, 4)
+    return res, d, dev, ms
+
+
+def decode_summary(r: dict) -> dict:
+    """The decode-sized workload's figures for the headline line."""
+    out = {"workload": r["config"]["workload"], "config": r["config"],
+           "ms_per_step": r["ms_per_step"], "value": r["value"], "unit": "tokens/s",
+           "graph_replay_ms": r["graph_replay_ms"], "kernels_ms": r["kernels_ms"],
+           "gate_up_roofline": r["roofline"]}
+    for key in ("step_hbm_gbs", "step_hbm_frac"):
+        if key in r:
+            out[key] = r[key]
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="mixtral")
+    ap.add_argument("--workload", default="dsv3_prefill",
+                    help="headline workload (default: the DeepSeek-V3-shaped prefill shard, "
+                         "the largest configuration)")
+    ap.add_argument("--decode-workload", default="dsv3_decode",
+                    help="decode-sized workload timed in the same run for the HBM figures")
+    ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--server-slots", type=int, default=0,
                     help="also time the server step over this many client slots holding the "
@@ -312,118 +471,33 @@ def main() -> int:
 
     import torch
 
-    from oracle import eaas_oracle as O
-    from paper_2509_17863_amd import eaas, synth
-    from paper_2509_17863_amd.device_io import to_device
-
     assert torch.cuda.is_available(), "no GPU"
-    wl = synth.WORKLOADS[args.workload]
-    d = synth.make_workload(args.workload)
-    dev = to_device(d)
-    T, H, I, E, k = d["T"], d["H"], d["I"], d["E"], d["k"]
-    act8 = bool(d.get("act8"))
-    wdt = (eaas.EAAS_FP8_E4M3_A8 if act8 else eaas.EAAS_FP8_E4M3) if d["wdtype"] == "fp8" \
-        else eaas.EAAS_BF16
-    ws = eaas.alloc_workspace(T, H, I, E, k, wdt)
-    out = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
-    counts = np.bincount(d["topk_ids"].ravel()[d["topk_ids"].ravel() >= 0], minlength=E)
-    alg = algorithmic(d, counts)
-
-    stream = torch.cuda.current_stream()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-
-    def step(ev=None):
-        if ev is None:
-            eaas.eaas_expert_forward(dev["x"], dev["topk_ids"], dev["topk_weights"],
-                                     dev["w_gate_up"], dev["w_down"], out, ws,
-                                     dev["w_gate_up_scale"], dev["w_down_scale"], act8=act8)
-        else:
-            eaas.eaas_expert_forward_profiled(dev["x"], dev["topk_ids"], dev["topk_weights"],
-                                              dev["w_gate_up"], dev["w_down"], out, ws,
-                                              dev["w_gate_up_scale"], dev["w_down_scale"],
-                                              events=ev, act8=act8)
-
     clocks_before = gpu_clocks()
-    for ev in evs:  # create the events before the timed region
-        for e in ev:
-            e.record(stream)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(evs[i])
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms = (t1 - t0) * 1e3 / args.steps
-
-    def mean_ms(a, b):
-        return float(np.mean([evs[i][a].elapsed_time(evs[i][b]) for i in range(args.steps)]))
-
-    # the step as the paper deploys it (§4.3): captured once in a graph, then
-    # replayed; the same kernels with no launches from the host per step
-    ms_graph, graph_stats = time_graph(step, args.steps, args.warmup)
+    r, d, dev, ms_eager = measure(args.workload, args.steps, args.warmup)
     clocks_after = gpu_clocks()
-
-    t_route, t_gu, t_dn, t_comb = mean_ms(0, 1), mean_ms(1, 2), mean_ms(2, 3), mean_ms(3, 4)
-    t_step_ev = mean_ms(0, 4)
-    # the gate/up launch's bound: HBM when its algorithmic intensity is below
-    # the ridge of the MFMA peak it runs on (fp8 x fp8 with fp8 activations,
-    # bf16 otherwise), the matrix cores above it
-    peak_flops = PEAK_FP8_TFLOPS if act8 else PEAK_BF16_TFLOPS
-    intensity = alg["gu_flops"] / alg["gu_bytes"]
-    hbm_bound = intensity < peak_flops * 1e12 / (PEAK_HBM_GBS * 1e9)
-    if act8 and not hbm_bound:
-        # fp8 x fp8 contraction: priced against the fp8 MFMA peak
-        achieved = alg["gu_flops"] / (t_gu * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_FP8_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP8_TFLOPS, 4), "traffic": None}
-    elif hbm_bound:
-        achieved = alg["gu_bytes"] / (t_gu * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
-    else:
-        achieved = alg["gu_flops"] / (t_gu * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None}
-    roof["traffic"] = measured_traffic(args.workload)
-    roof["traffic_unit"] = "bytes per launch"
-    roof["algorithmic_bytes"] = int(alg["gu_bytes"])
-    roof["kernel"] = gate_up_kernel_name(d)
     res = {
         "metric": "expert-FFN tokens/s",
-        "value": round(T / (ms_graph * 1e-3), 1),
+        "value": r["value"],
         "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_graph, 4),
+        "ms_per_step": r["ms_per_step"],
         "timing": "hipGraph replay of eaas_expert_forward (per-kernel times from an eager pass "
                   "with events in the same run)",
-        "graph_replay_ms": graph_stats,
-        "eager": {"ms_per_step": round(ms, 4), "value": round(T / (ms * 1e-3), 1),
-                  "graph_speedup": round(ms / ms_graph, 4)},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "fp8e4m3" if act8 else "bf16", "data": "synthetic",
-        "config": {"workload": args.workload, "T": T, "H": H, "I": I, "E": E, "k": k,
-                   "weights": d["wdtype"], "seed": wl.seed, "zipf": wl.zipf,
-                   "active_experts": int((counts > 0).sum()), "parallelism": "none (1 GPU)"},
-        "step_tflops": round(alg["flops"] / (ms_graph * 1e-3) / 1e12, 1),
-        "step_frac_bf16_peak": round(alg["flops"] / (ms_graph * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-        # the two grouped GEMMs alone: 6RHI over their summed event times
-        "gemm_tflops": round(alg["flops"] / ((t_gu + t_dn) * 1e-3) / 1e12, 1),
-        "gemm_frac_bf16_peak": round(alg["flops"] / ((t_gu + t_dn) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-        "kernels_ms": {"route": round(t_route, 4), "gate_up": round(t_gu, 4),
-                       "down": round(t_dn, 4), "combine": round(t_comb, 4),
-                       "step_events": round(t_step_ev, 4)},
-        "down_tflops": round(alg["dn_flops"] / (t_dn * 1e-3) / 1e12, 1),
-        "roofline": roof,
+        "data": "synthetic",
     }
+    res.update({key: v for key, v in r.items() if key not in res})
     if args.clients > 0:
-        res["segments"] = time_segments(d, dev, args.clients, args.steps, args.warmup, ms)
-    res["clocks_mhz"] = {"before": clocks_before, "after": clocks_after}
+        res["segments"] = time_segments(d, dev, args.clients, args.steps, args.warmup, ms_eager)
     if args.server_slots > 0:
-        res["server_step"] = time_server(d, dev, args.server_slots, args.steps, args.warmup, ms)
-    if hbm_bound:
-        res["step_hbm_gbs"] = round((alg["gu_bytes"] + alg["dn_bytes"]) / (ms_graph * 1e-3) / 1e9, 1)
+        res["server_step"] = time_server(d, dev, args.server_slots, args.steps, args.warmup,
+                                         ms_eager)
+    res["clocks_mhz"] = {"before": clocks_before, "after": clocks_after}
+    if not args.no_decode and args.decode_workload != args.workload:
+        del dev
+        torch.cuda.empty_cache()
+        rd, _, _, _ = measure(args.decode_workload, max(args.steps, 200), args.warmup)
+        res["decode"] = decode_summary(rd)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(d)
     print(json.dumps(res), flush=True)

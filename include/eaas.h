@@ -66,10 +66,12 @@ typedef struct eaas_shape {
 
 enum eaas_status {
   EAAS_OK = 0,
-  EAAS_ERR_INVALID_ARG = -1, /* null pointer, negative size, bad dtype, overlap */
+  EAAS_ERR_INVALID_ARG = -1, /* null pointer, negative size, bad dtype, overlap
+                                (k > E is valid: see eaas_route_permute) */
   EAAS_ERR_UNSUPPORTED = -2, /* H or I not a multiple of 128, E > 1024, k > 64,
                                 T*k >= 2^31 or sizes past 32-bit row indexing */
-  EAAS_ERR_WORKSPACE = -3,   /* ws NULL or smaller than eaas_workspace_bytes */
+  EAAS_ERR_WORKSPACE = -3,   /* ws NULL, misaligned or smaller than the entry
+                                point's eaas_workspace_bytes_for */
   EAAS_ERR_HIP = -4          /* a kernel launch was rejected by the runtime  */
 };
 
@@ -114,6 +116,20 @@ typedef struct eaas_routing {
  * library rejects. */
 size_t eaas_workspace_bytes(const eaas_shape *s, int w_dtype);
 
+/* Bytes of workspace one entry point needs for this shape and weight dtype:
+ *   EAAS_ENTRY_ROUTE_PERMUTE  eaas_route_permute (its histogram only; w_dtype
+ *                             is ignored beyond validation)
+ *   EAAS_ENTRY_FFN_GROUPED    eaas_expert_ffn_grouped (h, and for
+ *                             EAAS_FP8_E4M3_A8 the quantized x; no staging)
+ *   EAAS_ENTRY_FORWARD        eaas_expert_forward(_profiled), which is
+ *                             eaas_workspace_bytes
+ * Each is at most eaas_workspace_bytes(s, w_dtype).  Returns 0 for a shape or
+ * dtype the library rejects and for an unknown entry. */
+enum eaas_entry {
+  EAAS_ENTRY_ROUTE_PERMUTE = 0, EAAS_ENTRY_FFN_GROUPED = 1, EAAS_ENTRY_FORWARD = 2
+};
+size_t eaas_workspace_bytes_for(const eaas_shape *s, int w_dtype, int entry);
+
 /* Where a forward call leaves its intermediates inside the workspace (for
  * inspection and tests; the contents are those of the last call that used
  * the workspace, rows in the grouped order of the routing):
@@ -148,7 +164,10 @@ int eaas_quantize_rows_fp8(const void *x, int64_t rows, int32_t K, void *q, floa
 /* Token reorganisation + group-shrink (§3.3 Fig. 5, §4.1).
  *   topk_ids [T,k] int32   expert id per slot (payload `expert_id`, §3.2)
  *   r                      all five arrays written, bit-exact and deterministic
- * Needs ws of eaas_workspace_bytes(s, EAAS_BF16) bytes. */
+ * Needs ws of eaas_workspace_bytes_for(s, EAAS_BF16, EAAS_ENTRY_ROUTE_PERMUTE)
+ * bytes (a histogram of ceil(T*k/2048) x E ints); H and I only need to pass
+ * validation.  k may exceed E: slots whose ids name other servers' experts are
+ * skipped, so a server with fewer experts than a token has slots is valid. */
 int eaas_route_permute(const eaas_shape *s, const int32_t *topk_ids,
                        const eaas_routing *r, void *ws, size_t ws_bytes,
                        void *stream);
@@ -161,7 +180,8 @@ int eaas_route_permute(const eaas_shape *s, const int32_t *topk_ids,
  *   w_down     [E,H,I]  bf16 or fp8; w_down_scale [E,H/128,I/128] likewise
  *   y_perm     [R,H] fp32 output: row r = y_{e(r)}(x[perm[r]/k]), unweighted;
  *              rows >= offsets[E] are left untouched
- * Only experts listed in r->active are read. */
+ * Only experts listed in r->active are read.  Needs ws of
+ * eaas_workspace_bytes_for(s, w_dtype, EAAS_ENTRY_FFN_GROUPED) bytes. */
 int eaas_expert_ffn_grouped(const eaas_shape *s, const void *x,
                             const eaas_routing *r, const void *w_gate_up,
                             const float *w_gate_up_scale, const void *w_down,

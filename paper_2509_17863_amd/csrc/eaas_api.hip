@@ -20,8 +20,11 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 struct WsLayout {
   size_t hist, counts, offsets, perm, inv, active, h, stage, total;
   // fp8 activations: h held as hq [R,I] + hs [R,I/128] inside the h region,
-  // x quantized into xq [T,H] + xs [T,H/128] after the staging
+  // x quantized into xq [T,H] + xs [T,H/128] after it
   size_t hq, hs, xq, xs;
+  // bytes eaas_route_permute uses (the histogram) and eaas_expert_ffn_grouped
+  // uses (everything before the staging); the forward uses `total`
+  size_t route_total, ffn_total;
   // dynamic batch only: the requests gathered into one contiguous batch
   size_t x_cat, ids_cat, w_cat, seg_total;
 };
@@ -31,6 +34,7 @@ WsLayout layout(const eaas_shape& s, int w_dtype = EAAS_BF16) {
   WsLayout L{};
   size_t o = 0;
   L.hist = o;    o = align_up(o + (size_t)route_blocks((int)R) * s.E * 4);
+  L.route_total = o;
   L.counts = o;  o = align_up(o + (size_t)s.E * 4);
   L.offsets = o; o = align_up(o + (size_t)(s.E + 1) * 4);
   L.perm = o;    o = align_up(o + R * 4);
@@ -40,11 +44,12 @@ WsLayout layout(const eaas_shape& s, int w_dtype = EAAS_BF16) {
   L.hq = L.h;
   L.hs = align_up(L.h + R * s.I);
   o = align_up(std::max(L.h + R * s.I * 2, L.hs + R * (s.I / 128) * 4));
-  L.stage = o;   o = align_up(o + R * s.H * 4);
   if (w_dtype == EAAS_FP8_E4M3_A8) {
     L.xq = o;    o = align_up(o + (size_t)s.T * s.H);
     L.xs = o;    o = align_up(o + (size_t)s.T * (s.H / 128) * 4);
   }
+  L.ffn_total = o;
+  L.stage = o;   o = align_up(o + R * s.H * 4);
   L.total = o;
   L.x_cat = o;   o = align_up(o + (size_t)s.T * s.H * 2);
   L.ids_cat = o; o = align_up(o + R * 4);
@@ -128,6 +133,17 @@ size_t eaas_workspace_bytes(const eaas_shape* s, int w_dtype) {
   return layout(*s, w_dtype).total;
 }
 
+size_t eaas_workspace_bytes_for(const eaas_shape* s, int w_dtype, int entry) {
+  if (eaas_workspace_bytes(s, w_dtype) == 0) return 0;
+  const WsLayout L = layout(*s, w_dtype);
+  switch (entry) {
+    case EAAS_ENTRY_ROUTE_PERMUTE: return L.route_total;
+    case EAAS_ENTRY_FFN_GROUPED: return L.ffn_total;
+    case EAAS_ENTRY_FORWARD: return L.total;
+    default: return 0;
+  }
+}
+
 int eaas_workspace_region(const eaas_shape* s, int w_dtype, int region, size_t* offset,
                           size_t* bytes) {
   if (!offset || !bytes) return EAAS_ERR_INVALID_ARG;
@@ -176,7 +192,7 @@ int eaas_route_permute(const eaas_shape* s, const int32_t* topk_ids, const eaas_
   if (s->T == 0) return EAAS_OK;
   if (!topk_ids || !routing_ok(r)) return EAAS_ERR_INVALID_ARG;
   const WsLayout L = layout(*s);
-  if (!ws || !aligned16(ws) || ws_bytes < L.total) return EAAS_ERR_WORKSPACE;
+  if (!ws || !aligned16(ws) || ws_bytes < L.route_total) return EAAS_ERR_WORKSPACE;
   char* base = static_cast<char*>(ws);
   return hip_status(launch_route_permute(topk_ids, s->T * s->k, s->E, *r,
                                          reinterpret_cast<int32_t*>(base + L.hist),
@@ -195,7 +211,7 @@ int eaas_expert_ffn_grouped(const eaas_shape* s, const void* x, const eaas_routi
     return EAAS_ERR_INVALID_ARG;
   if ((st = check_dtype_shape(s, w_dtype)) != EAAS_OK) return st;
   const WsLayout L = layout(*s, w_dtype);
-  if (!ws || !aligned16(ws) || ws_bytes < L.total) return EAAS_ERR_WORKSPACE;
+  if (!ws || !aligned16(ws) || ws_bytes < L.ffn_total) return EAAS_ERR_WORKSPACE;
   char* base = static_cast<char*>(ws);
   FfnArgs a{};
   a.T = s->T; a.H = s->H; a.I = s->I; a.E = s->E; a.k = s->k;

@@ -22,17 +22,20 @@ __all__ = [
     "eaas_server_workspace_bytes", "alloc_server_workspace", "slot_table", "layer_table",
     "eaas_server_step", "eaas_quantize_rows_fp8", "eaas_workspace_region", "workspace_view",
     "EAAS_WS_H", "EAAS_WS_HQ", "EAAS_WS_HS", "EAAS_WS_XQ", "EAAS_WS_XS", "EAAS_WS_STAGE",
+    "eaas_workspace_bytes_for", "EAAS_ENTRY_ROUTE_PERMUTE", "EAAS_ENTRY_FFN_GROUPED",
+    "EAAS_ENTRY_FORWARD",
 ]
 
 EAAS_OK = 0
 EAAS_BF16, EAAS_FP8_E4M3, EAAS_FP32, EAAS_FP8_E4M3_A8 = 0, 1, 2, 3
 EAAS_SLOT_EMPTY, EAAS_SLOT_READY, EAAS_SLOT_DONE, EAAS_SLOT_OFFLINE = 0, 1, 2, 3
 EAAS_WS_H, EAAS_WS_HQ, EAAS_WS_HS, EAAS_WS_XQ, EAAS_WS_XS, EAAS_WS_STAGE = range(6)
+EAAS_ENTRY_ROUTE_PERMUTE, EAAS_ENTRY_FFN_GROUPED, EAAS_ENTRY_FORWARD = range(3)
 EXPORTED = ("eaas_workspace_bytes", "eaas_route_permute", "eaas_expert_ffn_grouped",
             "eaas_unpermute_combine", "eaas_expert_forward", "eaas_expert_forward_profiled",
             "eaas_status_string", "eaas_segments_workspace_bytes",
             "eaas_expert_forward_segments", "eaas_server_workspace_bytes", "eaas_server_step",
-            "eaas_quantize_rows_fp8", "eaas_workspace_region")
+            "eaas_quantize_rows_fp8", "eaas_workspace_region", "eaas_workspace_bytes_for")
 
 _LIB_PATH = Path(__file__).resolve().parent / "libeaas.so"
 _lib = None
@@ -70,6 +73,8 @@ def lib() -> ctypes.CDLL:
         sp, rp = ctypes.POINTER(_Shape), ctypes.POINTER(_Routing)
         L.eaas_workspace_bytes.argtypes = [sp, i32]
         L.eaas_workspace_bytes.restype = sz
+        L.eaas_workspace_bytes_for.argtypes = [sp, i32, i32]
+        L.eaas_workspace_bytes_for.restype = sz
         L.eaas_route_permute.argtypes = [sp, vp, rp, vp, sz, vp]
         L.eaas_route_permute.restype = i32
         L.eaas_expert_ffn_grouped.argtypes = [sp, vp, rp, vp, vp, vp, vp, i32, vp, vp, sz, vp]
@@ -172,6 +177,11 @@ def eaas_quantize_rows_fp8(x: torch.Tensor, q: torch.Tensor, s: torch.Tensor, st
 def eaas_workspace_bytes(T, H, I, E, k, w_dtype=EAAS_BF16) -> int:
     s = _shape(T, H, I, E, k)
     return int(lib().eaas_workspace_bytes(ctypes.byref(s), int(w_dtype)))
+
+
+def eaas_workspace_bytes_for(T, H, I, E, k, w_dtype, entry) -> int:
+    s = _shape(T, H, I, E, k)
+    return int(lib().eaas_workspace_bytes_for(ctypes.byref(s), int(w_dtype), int(entry)))
 
 
 def alloc_workspace(T, H, I, E, k, w_dtype=EAAS_BF16, device="cuda") -> torch.Tensor:

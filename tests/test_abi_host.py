@@ -225,3 +225,50 @@ def test_quantize_rows_rejects_bad_args():
     assert L.eaas_quantize_rows_fp8(FAKE + 8, 4, 128, FAKE, FAKE, None) == -1
     assert L.eaas_quantize_rows_fp8(FAKE, 4, 128, None, FAKE, None) == -1
     assert L.eaas_quantize_rows_fp8(None, 0, 128, None, None, None) == 0
+
+
+@pytest.mark.parametrize("T,H,I,E,k,wdt", [(64, 256, 128, 8, 2, 0), (16384, 7168, 2048, 32, 8, 0),
+                                          (256, 7168, 2048, 32, 8, 1), (300, 512, 256, 6, 2, 3),
+                                          (5000, 2048, 768, 128, 8, 0)])
+def test_workspace_bytes_per_entry(T, H, I, E, k, wdt):
+    """route_permute needs its histogram, ffn_grouped everything but the
+    staging, the forward the whole workspace."""
+    f = lambda e: eaas.eaas_workspace_bytes_for(T, H, I, E, k, wdt, e)  # noqa: E731
+    route, ffn, fwd = (f(eaas.EAAS_ENTRY_ROUTE_PERMUTE), f(eaas.EAAS_ENTRY_FFN_GROUPED),
+                       f(eaas.EAAS_ENTRY_FORWARD))
+    R = T * k
+    assert fwd == eaas.eaas_workspace_bytes(T, H, I, E, k, wdt)
+    assert route == -(-((R + 2047) // 2048) * E * 4 // 256) * 256
+    assert route < ffn < fwd
+    assert ffn >= R * I * 2 + 2 * R * 4
+    assert fwd - ffn >= R * H * 4                 # the fp32 staging is the forward's alone
+    assert eaas.eaas_workspace_bytes_for(T, H, I, E, k, wdt, 7) == 0
+    assert eaas.eaas_workspace_bytes_for(T, 200, I, E, k, wdt, 0) == 0
+
+
+def test_entry_workspace_minimums_enforced():
+    L = eaas.lib()
+    s = shape()
+    r = _routing()
+    route = eaas.eaas_workspace_bytes_for(64, 256, 128, 8, 2, 0, eaas.EAAS_ENTRY_ROUTE_PERMUTE)
+    ffn = eaas.eaas_workspace_bytes_for(64, 256, 128, 8, 2, 0, eaas.EAAS_ENTRY_FFN_GROUPED)
+    assert L.eaas_route_permute(ctypes.byref(s), FAKE, ctypes.byref(r), FAKE, route - 1,
+                                None) == -3
+    assert L.eaas_route_permute(ctypes.byref(s), FAKE, ctypes.byref(r), FAKE + 8, route,
+                                None) == -3   # misaligned workspace
+    assert L.eaas_expert_ffn_grouped(ctypes.byref(s), FAKE, ctypes.byref(r), FAKE, None, FAKE,
+                                     None, 0, FAKE, FAKE, ffn - 1, None) == -3
+
+
+def test_k_above_E_is_a_valid_shape():
+    """A server may hold fewer experts than a token has slots (the other
+    slots name experts of other servers and are skipped): k > E passes
+    validation, up to the k <= 64 limit."""
+    assert eaas.eaas_workspace_bytes(64, 256, 128, 3, 8) > 0
+    assert eaas.eaas_workspace_bytes(64, 256, 128, 1, 64) > 0
+    assert eaas.eaas_workspace_bytes(64, 256, 128, 1, 65) == 0
+    L = eaas.lib()
+    s = shape(E=3, k=8)
+    r = _routing()
+    # validation passes the shape and stops at the missing workspace
+    assert L.eaas_route_permute(ctypes.byref(s), FAKE, ctypes.byref(r), None, 0, None) == -3

@@ -173,11 +173,30 @@ def test_forward_hand_fixture(gpu):
 
 
 # ---------------------------------------------------------------- forward, full size
-@pytest.mark.timeout(600)
+def oracle_out_all_tokens(d, chunk=2048):
+    """The oracle's fp64 output for every token of a full-size batch, computed
+    over sub-batches of `chunk` tokens (a token's outputs depend on that token
+    alone) with each expert's weights converted to fp64 once."""
+    E, T = d["E"], d["T"]
+    w64 = ([], [])
+    for e in range(E):
+        wg, wu, wd = O.expert_weights_f64(d, e)
+        w64[0].append(np.concatenate([wg, wu]))
+        w64[1].append(wd)
+    out = np.empty((T, d["H"]), dtype=np.float64)
+    for a in range(0, T, chunk):
+        b = min(T, a + chunk)
+        out[a:b] = O.expert_forward(O.sub_batch(d, np.arange(a, b)), weights=w64)["out"]
+    return out
+
+
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", list(synth.WORKLOADS))
-def test_forward_workload_sampled(gpu, name):
+def test_forward_workload_all_tokens(gpu, name):
+    """Every token of every full-size workload against the oracle (fp32
+    output), plus determinism and the bf16 output being RNE of the fp32 one."""
     if synth.WORKLOADS[name].act8:
-        pytest.skip("fp8-activation workloads: tests/test_gpu_w8a8.py")
+        pytest.skip("fp8-activation workloads: tests/test_gpu_w8a8.py (all tokens there too)")
     d = synth.make_workload(name)
     T, k = d["T"], d["k"]
     dev = to_device(d)
@@ -193,12 +212,110 @@ def test_forward_workload_sampled(gpu, name):
     ref16 = torch.from_numpy(o32).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     assert np.array_equal(bf16_tensor_to_bits(out16), ref16)
     assert np.isfinite(o32).all()
-    # sampled tokens, the oracle on that sub-batch (tokens are independent)
-    rng = np.random.default_rng(1234)
-    n = min(T, 48)
-    tokens = np.sort(rng.choice(T, size=n, replace=False))
-    ref = O.expert_forward(O.sub_batch(d, tokens))["out"]
-    check_close(o32[tokens], ref, f"workload {name} ({n} sampled tokens)")
+    del dev, out32, out16, again
+    say("forward workload", name, "oracle on all", T, "tokens")
+    ref = oracle_out_all_tokens(d)
+    check_close(o32, ref, f"workload {name} (all {T} tokens)")
+
+
+# ------------------------------------------------- exact h stage (integer data)
+def integer_bits(rng, shape, p, fp8=False):
+    """Entries -1, 0, +1 with P(nonzero) = p, as bf16 (or e4m3fn) bits: exact
+    in either format, and every fp32 sum of them is exact."""
+    u = rng.random(shape, dtype=np.float32)
+    if fp8:
+        one, neg = np.uint8(0x38), np.uint8(0xB8)       # e4m3fn +1.0, -1.0
+        return np.where(u < p / 2, neg, np.where(u < p, one, np.uint8(0)))
+    one, neg = np.uint16(0x3F80), np.uint16(0xBF80)     # bf16 +1.0, -1.0
+    return np.where(u < p / 2, neg, np.where(u < p, one, np.uint16(0)))
+
+
+def integer_workload(name, seed=77):
+    """The workload's batch and routing with x and weights replaced by
+    sparse integers (fp8 weights keep scales of exactly 1): G and U are then
+    integers below 2^24, exact in any fp32 summation order.  The density
+    gives G a standard deviation near 8, across the curved part of silu."""
+    d = synth.make_workload(name, weights=False)
+    T, H, I, E = d["T"], d["H"], d["I"], d["E"]
+    fp8 = synth.WORKLOADS[name].wdtype == "fp8"
+    rng = np.random.default_rng(seed)
+    p = float(np.sqrt(64.0 / H))
+    d["x"] = integer_bits(rng, (T, H), p)
+    d["w_gate_up"] = np.stack([integer_bits(rng, (2 * I, H), p, fp8) for _ in range(E)])
+    d["w_down"] = np.stack([integer_bits(rng, (H, I), np.sqrt(64.0 / I), fp8) for _ in range(E)])
+    d["w_gate_up_scale"] = np.ones((E, 2 * I // 128, H // 128), np.float32) if fp8 else None
+    d["w_down_scale"] = np.ones((E, H // 128, I // 128), np.float32) if fp8 else None
+    d["wdtype"] = "fp8" if fp8 else "bf16"
+    return d
+
+
+# The kernel evaluates silu(g) * u with the hardware exp and reciprocal: for
+# |g| <= 88 its fp32 value lies within 2^-17 (relative) of the exact one.
+# Where [v (1 - 2^-16), v (1 + 2^-16)] holds a bf16 rounding boundary either
+# rounding is accepted; everywhere else h must match exactly.
+H_REL = 2.0 ** -16
+
+
+def exact_h_candidates(g, u):
+    """bf16 values h may take for exact integer g, u (fp64 arrays)."""
+    with np.errstate(over="ignore"):
+        v = g / (1.0 + np.exp(-g)) * u
+    lo = O.bf16_to_f32(O.f32_to_bf16_rne((v * (1 - H_REL)).astype(np.float32)))
+    hi = O.bf16_to_f32(O.f32_to_bf16_rne((v * (1 + H_REL)).astype(np.float32)))
+    return lo, hi
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["mixtral", "qwen3", "dsv3_prefill", "dsv3_decode"])
+def test_gate_up_h_exact_on_integer_data(gpu, name):
+    """Full-size gate/up stage with integer x and weights: every h of the
+    grouped layout equals the exactly computed value's bf16 rounding (either
+    neighbour only where the exact value is within 2^-16 of a rounding
+    boundary).  An indexing slip anywhere in the grouped GEMM (a wrong row,
+    column, expert or K tile) moves G by whole integers and fails here."""
+    d = integer_workload(name)
+    T, H, I, E, k = d["T"], d["H"], d["I"], d["E"], d["k"]
+    wdt = eaas.EAAS_FP8_E4M3 if d["wdtype"] == "fp8" else eaas.EAAS_BF16
+    dev = to_device(d)
+    say("exact h", name, d["wdtype"])
+    ws = eaas.alloc_workspace(T, H, I, E, k, wdt)
+    out = torch.empty((T, H), dtype=torch.float32, device="cuda")
+    eaas.eaas_expert_forward(dev["x"], dev["topk_ids"], dev["topk_weights"], dev["w_gate_up"],
+                             dev["w_down"], out, ws, dev["w_gate_up_scale"], dev["w_down_scale"])
+    torch.cuda.synchronize()
+    h = eaas.workspace_view(ws, T, H, I, E, k, wdt, eaas.EAAS_WS_H).cpu().numpy().view(np.uint16)
+    h = O.bf16_to_f32(h.reshape(T * k, I))
+    del dev, ws, out
+    rt = O.route_permute(d["topk_ids"], E)
+    off, perm = rt["offsets"], rt["perm"]
+    x = O.bf16_to_f32(d["x"])
+    n_amb = n_all = 0
+    for e in range(E):
+        r0, r1 = int(off[e]), int(off[e + 1])
+        if r1 == r0:
+            continue
+        if d["wdtype"] == "fp8":
+            wgu = O.e4m3fn_to_f32(d["w_gate_up"][e])
+        else:
+            wgu = O.bf16_to_f32(d["w_gate_up"][e])
+        a = x[perm[r0:r1] // k]
+        g = (a @ wgu[:I].T).astype(np.float64)   # integers < 2^24: exact in fp32
+        u = (a @ wgu[I:].T).astype(np.float64)
+        # (below -88 the kernel's exp overflows to a silu of 0: the data
+        # never reach it, g has a standard deviation near 8)
+        assert np.abs(g).max() < 2 ** 24 and g.min() > -80
+        lo, hi = exact_h_candidates(g, u)
+        got = h[r0:r1]
+        ok = (got == lo) | (got == hi)
+        bad = np.argwhere(~ok)
+        assert bad.size == 0, (f"expert {e}: {len(bad)} h values wrong, first (row, col) "
+                               f"{bad[:4].tolist()}: got {got[tuple(bad[0])]}, "
+                               f"want {lo[tuple(bad[0])]} or {hi[tuple(bad[0])]}")
+        n_amb += int((lo != hi).sum())
+        n_all += lo.size
+    say(f"exact h {name}: {n_all} values equal; {n_amb} near a rounding boundary "
+        f"({n_amb / max(n_all, 1):.2e})")
+    assert n_all == T * k * I
 
 
 # ---------------------------------------------------------------- properties
@@ -348,3 +465,80 @@ def test_empty_batch_is_noop(gpu):
     ws = torch.empty(256, dtype=torch.uint8, device="cuda")
     eaas.eaas_expert_forward(x, ids, w, wgu, wd, out, ws)
     torch.cuda.synchronize()
+
+
+# ------------------------------------------- poisoned workspace, output canaries
+CANARY_F32 = np.uint32(0x7FA5A5A5)   # a NaN payload no kernel writes
+
+
+@pytest.mark.parametrize("wdtype", ["bf16", "fp8"])
+def test_poisoned_workspace_and_canaries(gpu, wdtype):
+    """The step rebuilds every intermediate itself: a workspace filled with
+    NaN bytes (-1 as int32) gives the clean run's result bit for bit.  Rows
+    of guard memory around the output and bytes past the workspace the call
+    was given keep their canary values."""
+    d = synth.make_inputs(700, 512, 384, 7, 3, 81, zipf=1.3, wdtype=wdtype)
+    d["topk_ids"][::11, 1] = -1
+    T, H, I, E, k = d["T"], d["H"], d["I"], d["E"], d["k"]
+    wdt = eaas.EAAS_FP8_E4M3 if wdtype == "fp8" else eaas.EAAS_BF16
+    dev = to_device(d)
+    say("poisoned workspace", wdtype)
+    clean = forward(dev, k).cpu().numpy()
+    n = eaas.eaas_workspace_bytes(T, H, I, E, k, wdt)
+    G = 8
+    ws_big = torch.full((n + 4096,), 0xFF, dtype=torch.uint8, device="cuda")
+    ws_big[n:] = 0xA5
+    guard = torch.from_numpy(np.full((T + 2 * G, H), CANARY_F32, np.uint32)).cuda()
+    out = guard.view(torch.float32)[G:G + T]
+    assert out.is_contiguous()
+    eaas.eaas_expert_forward(dev["x"], dev["topk_ids"], dev["topk_weights"], dev["w_gate_up"],
+                             dev["w_down"], out, ws_big[:n], dev["w_gate_up_scale"],
+                             dev["w_down_scale"])
+    torch.cuda.synchronize()
+    g = guard.cpu().numpy()
+    assert np.all(g[:G] == CANARY_F32) and np.all(g[G + T:] == CANARY_F32), "output guard rows"
+    assert np.array_equal(g[G:G + T], clean.view(np.uint32)), "poisoned workspace changed the result"
+    assert torch.all(ws_big[n:] == 0xA5).item(), "bytes past the workspace were written"
+    # the modular entry points with workspaces of exactly their own size
+    nr = eaas.eaas_workspace_bytes_for(T, H, I, E, k, wdt, eaas.EAAS_ENTRY_ROUTE_PERMUTE)
+    nf = eaas.eaas_workspace_bytes_for(T, H, I, E, k, wdt, eaas.EAAS_ENTRY_FFN_GROUPED)
+    ws_r = torch.full((nr + 256,), 0xA5, dtype=torch.uint8, device="cuda")
+    ws_f = torch.full((nf + 256,), 0xFF, dtype=torch.uint8, device="cuda")
+    ws_f[nf:] = 0xA5
+    r = eaas.alloc_routing(T, k, E)
+    eaas.eaas_route_permute(dev["topk_ids"], E, r, ws_r[:nr], H=H, I=I)
+    yg = torch.from_numpy(np.full((T * k + 2 * G, H), CANARY_F32, np.uint32)).cuda()
+    y = yg.view(torch.float32)[G:G + T * k]
+    eaas.eaas_expert_ffn_grouped(dev["x"], r, dev["w_gate_up"], dev["w_down"], y, ws_f[:nf], k,
+                                 dev["w_gate_up_scale"], dev["w_down_scale"])
+    out2 = torch.empty((T, H), dtype=torch.float32, device="cuda")
+    eaas.eaas_unpermute_combine(y, r, dev["topk_weights"], out2, E, I=I)
+    torch.cuda.synchronize()
+    assert torch.all(ws_r[nr:] == 0xA5).item() and torch.all(ws_f[nf:] == 0xA5).item()
+    ygn = yg.cpu().numpy()
+    R_valid = int((d["topk_ids"] >= 0).sum())
+    assert np.all(ygn[:G] == CANARY_F32) and np.all(ygn[G + T * k:] == CANARY_F32)
+    # rows past the valid slots are left untouched
+    assert np.all(ygn[G + R_valid:G + T * k] == CANARY_F32)
+    assert np.array_equal(out2.cpu().numpy().view(np.uint32), clean.view(np.uint32))
+
+
+def test_forward_k_above_E(gpu):
+    """A server with fewer experts than a token has slots: the slots naming
+    other servers' experts are skipped, duplicate ids count twice."""
+    rng = np.random.default_rng(82)
+    d = synth.make_inputs(300, 256, 256, 3, 2, 82, wdtype="bf16")
+    T, E, k = d["T"], d["E"], 8
+    extra = rng.choice(np.array([-1, 3, 9], np.int32), size=(T, k - 2))
+    extra = np.where(rng.random((T, k - 2)) < 0.3, d["topk_ids"][:, :1], extra).astype(np.int32)
+    d["topk_ids"] = np.ascontiguousarray(np.concatenate([d["topk_ids"], extra], 1))
+    d["topk_weights"] = np.ascontiguousarray(np.concatenate(
+        [d["topk_weights"], rng.random((T, k - 2)).astype(np.float32)], 1))
+    d["k"] = k
+    ref = O.expert_forward(d)
+    say("forward k > E")
+    r = eaas.alloc_routing(T, k, E)
+    out = forward(to_device(d), k, routing=r)
+    torch.cuda.synchronize()
+    assert_routing_equal({key: v.cpu().numpy() for key, v in r.items()}, ref["routing"], T * k, E)
+    check_close(out.cpu().numpy(), ref["out"], "k=8 > E=3")

@@ -108,6 +108,23 @@ def forward_layer_concat(slots, members, counts, lw, act8=False):
     return bf16_tensor_to_bits(out)
 
 
+def check_concat_w8a8(slots, members, counts, lw, ref_bits):
+    """fp8 activations: the concatenated requests' step against the
+    fp8-activation oracle, stage by stage on every token (fp32 output); the
+    server's bf16 rows are the round to nearest even of that fp32 output."""
+    from test_gpu_w8a8 import check_step as check_step_a8, forward_a8
+
+    T = int(sum(counts[b] for b in members))
+    d = dict(lw, T=T, H=H, I=I, E=E, k=K,
+             x=np.concatenate([slots[b]["x"][: counts[b]] for b in members]),
+             topk_ids=np.concatenate([slots[b]["topk_ids"][: counts[b]] for b in members]),
+             topk_weights=np.concatenate([slots[b]["topk_weights"][: counts[b]] for b in members]))
+    got, ws = forward_a8(d)
+    check_step_a8(d, got, ws, f"server step fp8 activations, {len(members)} requests")
+    rne = torch.from_numpy(got.astype(np.float32)).to(torch.bfloat16)
+    assert np.array_equal(bf16_tensor_to_bits(rne), ref_bits)
+
+
 def check_step(srv, before):
     """Compare the server's state after a step with the oracle's step from
     the state `before` (list of slot dicts as they were)."""
@@ -126,6 +143,8 @@ def check_step(srv, before):
         if not members:
             continue
         ref = forward_layer_concat(before, members, counts, lw, srv.act8)
+        if srv.act8:
+            check_concat_w8a8(before, members, counts, lw, ref)
         p = 0
         for b in members:
             n = int(counts[b])

@@ -274,6 +274,37 @@ def test_grouped_matches_brute_force(kw):
     assert np.abs(res["out"] - bf).max() <= 1e-12 * rms
 
 
+def widen_slots(d, k_new, seed=0):
+    """The request with k_new > E slots per token: the original slots, plus
+    slots naming other servers' experts (-1, E, E + 3) and duplicates of valid
+    ids, shuffled across the slot positions of each token."""
+    rng = np.random.default_rng(seed)
+    T, k = d["topk_ids"].shape
+    E = d["E"]
+    extra = rng.choice(np.array([-1, E, E + 3], np.int32), size=(T, k_new - k))
+    dup = rng.random((T, k_new - k)) < 0.3
+    extra = np.where(dup, d["topk_ids"][:, :1], extra).astype(np.int32)
+    ids = np.concatenate([d["topk_ids"], extra], axis=1)
+    w = np.concatenate([d["topk_weights"], rng.random((T, k_new - k)).astype(np.float32)], axis=1)
+    order = np.argsort(rng.random((T, k_new)), axis=1)
+    d2 = dict(d, k=k_new, topk_ids=np.take_along_axis(ids, order, 1),
+              topk_weights=np.take_along_axis(w, order, 1))
+    return d2
+
+
+def test_k_above_E_matches_brute_force():
+    # a server holding fewer experts than a token has slots: the slots naming
+    # other servers' experts are skipped, duplicates count twice
+    d = widen_slots(small_inputs(T=29, E=3, k=2, seed=17), k_new=8, seed=5)
+    assert d["k"] > d["E"]
+    res = O.expert_forward(d)
+    ids = d["topk_ids"]
+    assert res["routing"]["offsets"][-1] == int(((ids >= 0) & (ids < d["E"])).sum())
+    bf = O.brute_force_tokens(d, range(d["T"]))
+    rms = np.sqrt((bf ** 2).mean())
+    assert np.abs(res["out"] - bf).max() <= 1e-12 * rms
+
+
 def test_masked_token_is_zero_and_masked_slots_skipped():
     d = small_inputs(T=12, E=4, k=2, seed=21)
     d["topk_ids"][3] = [-1, 4]
