@@ -50,8 +50,13 @@ def post_async(srv, b, st):
     srv.dev[b][0].fill_(eaas.EAAS_SLOT_READY)
 
 
-@pytest.mark.parametrize("delay", [0, 1, 2, 3, 5, 8, 13])
-def test_late_write_is_answered_whole_or_left_ready(gpu, delay):
+@pytest.mark.parametrize("client_first", [False, True])
+@pytest.mark.parametrize("delay", [0, 2, 5, 13])
+def test_late_write_is_answered_whole_or_left_ready(gpu, delay, client_first):
+    """Which of the two outcomes occurs depends on when the runtime runs the
+    two streams' work (they may share a hardware queue, which then runs them
+    in submission order): the client's post is submitted after the step, or
+    (client_first) before it, each behind `delay` matrix products."""
     layers = make_layers(1, seed=90)
     # slot 2 starts empty; its client posts while the step may be running
     specs = [(1, 0, 100, 128), (1, 0, 90, 96), (0, 0, 0, 64), (1, 0, 60, 64)]
@@ -64,16 +69,23 @@ def test_late_write_is_answered_whole_or_left_ready(gpu, delay):
     big = torch.randn(2048, 2048, device="cuda")
     before = snapshot(srv.slots)
     torch.cuda.synchronize()
-    say("late write, delay", delay)
+    say("late write, delay", delay, "client first" if client_first else "server first")
     sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
-    with torch.cuda.stream(sa):
-        for _ in range(4):
-            big @ big
-        srv.step(sa)
-    with torch.cuda.stream(sb):
-        for _ in range(delay):
-            big @ big
-        post_async(srv, 2, st)
+
+    def server():
+        with torch.cuda.stream(sa):
+            for _ in range(4):
+                big @ big
+            srv.step(sa)
+
+    def client():
+        with torch.cuda.stream(sb):
+            for _ in range(delay):
+                big @ big
+            post_async(srv, 2, st)
+
+    for f in ((client, server) if client_first else (server, client)):
+        f()
     torch.cuda.synchronize()
     flag = int(srv.dev[2][0].item())
     assert flag in (eaas.EAAS_SLOT_READY, eaas.EAAS_SLOT_DONE), flag
