@@ -342,6 +342,37 @@ int eaas_server_step(const eaas_shape *s, const eaas_slot *slots, int n_slots,
                      const eaas_layer_weights *layers, int n_layers, int w_dtype,
                      void *ws, size_t ws_bytes, void *stream);
 
+/*
+ * For callers that cannot allocate device memory: code under hipGraph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  eaas_expert_forward
+ * with the caller's workspace replaced by a library-owned device array of
+ * EAAS_NOALLOC_SCRATCH_BYTES bytes per GPU: static device memory that every
+ * GPU the library is loaded on holds until the process ends.  The call itself
+ * allocates and frees nothing.
+ *   Same arguments and results as eaas_expert_forward (bitwise), without
+ *   ws / ws_bytes.  The array used is that of the device current at the call
+ *   (hipGetDevice), which must be the device `stream` belongs to.
+ *   A shape that needs more, eaas_workspace_bytes(s, w_dtype) >
+ *   EAAS_NOALLOC_SCRATCH_BYTES (80 MiB: it holds the 256-token, H 7168, I 2048,
+ *   32-expert, top-8 decode step with fp8 or bf16 weights), returns
+ *   EAAS_ERR_WORKSPACE and enqueues nothing; other errors as in
+ *   eaas_expert_forward.
+ *   Every call on one GPU shares that GPU's array, which keeps the last
+ *   call's intermediates (each call rebuilds everything it reads, so nothing
+ *   has to start at zero).  Calls that overlap in time on one GPU (on
+ *   different streams, or from several host threads) race on the array and
+ *   give undefined results: serialise them, e.g. on one stream.
+ */
+#define EAAS_NOALLOC_SCRATCH_BYTES (80u << 20)
+int eaas_expert_forward_noalloc(const eaas_shape *s, const void *x,
+                                const int32_t *topk_ids,
+                                const float *topk_weights,
+                                const void *w_gate_up,
+                                const float *w_gate_up_scale,
+                                const void *w_down, const float *w_down_scale,
+                                int w_dtype, void *out, int out_dtype,
+                                const eaas_routing *r, void *stream);
+
 /* Static, human-readable name of a status code. */
 const char *eaas_status_string(int status);
 

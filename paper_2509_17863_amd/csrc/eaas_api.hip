@@ -5,6 +5,8 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <atomic>
+#include <mutex>
 
 #include "common.h"
 #include "internal.h"
@@ -482,6 +484,61 @@ int eaas_server_step(const eaas_shape* s, const eaas_slot* slots, int n_slots,
     if (e != hipSuccess) return EAAS_ERR_HIP;
   }
   return hip_status(launch_slot_complete(slots, n_slots, taken, hs));
+}
+
+}  // extern "C"
+
+namespace {
+
+// Library-owned scratch of the allocation-free forward: static device memory,
+// one copy per GPU the library is loaded on.  In host code `scratch` only
+// names the symbol; its device address is taken once per device with
+// hipGetSymbolAddress and used from then on.
+static __device__ __align__(256) char scratch[EAAS_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// The scratch array's address on the current device (hipGetSymbolAddress on
+// the first call there, with that device current; cached afterwards).
+int scratch_on_current_device(void** ptr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return EAAS_ERR_HIP;
+  void* p = g_scratch[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return EAAS_ERR_HIP;
+      g_scratch[dev].store(p, std::memory_order_release);
+    }
+  }
+  *ptr = p;
+  return EAAS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int eaas_expert_forward_noalloc(const eaas_shape* s, const void* x, const int32_t* topk_ids,
+                                const float* topk_weights, const void* w_gate_up,
+                                const float* w_gate_up_scale, const void* w_down,
+                                const float* w_down_scale, int w_dtype, void* out, int out_dtype,
+                                const eaas_routing* r, void* stream) {
+  int st = check_shape(s);
+  if (st != EAAS_OK) return st;
+  if (s->T == 0) return EAAS_OK;
+  const size_t need = eaas_workspace_bytes(s, w_dtype);
+  if (need == 0) return check_dtype_shape(s, w_dtype) != EAAS_OK ? EAAS_ERR_UNSUPPORTED
+                                                                  : EAAS_ERR_INVALID_ARG;
+  if (need > (size_t)EAAS_NOALLOC_SCRATCH_BYTES) return EAAS_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if ((st = scratch_on_current_device(&ws)) != EAAS_OK) return st;
+  return eaas_expert_forward_profiled(s, x, topk_ids, topk_weights, w_gate_up, w_gate_up_scale,
+                                      w_down, w_down_scale, w_dtype, out, out_dtype, r, ws,
+                                      (size_t)EAAS_NOALLOC_SCRATCH_BYTES, stream, nullptr);
 }
 
 const char* eaas_status_string(int status) {

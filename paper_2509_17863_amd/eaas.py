@@ -23,7 +23,7 @@ __all__ = [
     "eaas_server_step", "eaas_quantize_rows_fp8", "eaas_workspace_region", "workspace_view",
     "EAAS_WS_H", "EAAS_WS_HQ", "EAAS_WS_HS", "EAAS_WS_XQ", "EAAS_WS_XS", "EAAS_WS_STAGE",
     "eaas_workspace_bytes_for", "EAAS_ENTRY_ROUTE_PERMUTE", "EAAS_ENTRY_FFN_GROUPED",
-    "EAAS_ENTRY_FORWARD",
+    "EAAS_ENTRY_FORWARD", "eaas_expert_forward_noalloc", "EAAS_NOALLOC_SCRATCH_BYTES",
 ]
 
 EAAS_OK = 0
@@ -31,11 +31,13 @@ EAAS_BF16, EAAS_FP8_E4M3, EAAS_FP32, EAAS_FP8_E4M3_A8 = 0, 1, 2, 3
 EAAS_SLOT_EMPTY, EAAS_SLOT_READY, EAAS_SLOT_DONE, EAAS_SLOT_OFFLINE = 0, 1, 2, 3
 EAAS_WS_H, EAAS_WS_HQ, EAAS_WS_HS, EAAS_WS_XQ, EAAS_WS_XS, EAAS_WS_STAGE = range(6)
 EAAS_ENTRY_ROUTE_PERMUTE, EAAS_ENTRY_FFN_GROUPED, EAAS_ENTRY_FORWARD = range(3)
+EAAS_NOALLOC_SCRATCH_BYTES = 80 << 20
 EXPORTED = ("eaas_workspace_bytes", "eaas_route_permute", "eaas_expert_ffn_grouped",
             "eaas_unpermute_combine", "eaas_expert_forward", "eaas_expert_forward_profiled",
             "eaas_status_string", "eaas_segments_workspace_bytes",
             "eaas_expert_forward_segments", "eaas_server_workspace_bytes", "eaas_server_step",
-            "eaas_quantize_rows_fp8", "eaas_workspace_region", "eaas_workspace_bytes_for")
+            "eaas_quantize_rows_fp8", "eaas_workspace_region", "eaas_workspace_bytes_for",
+            "eaas_expert_forward_noalloc")
 
 _LIB_PATH = Path(__file__).resolve().parent / "libeaas.so"
 _lib = None
@@ -86,6 +88,9 @@ def lib() -> ctypes.CDLL:
         L.eaas_expert_forward_profiled.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32,
                                                    rp, vp, sz, vp, vp]
         L.eaas_expert_forward_profiled.restype = i32
+        L.eaas_expert_forward_noalloc.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32,
+                                                  rp, vp]
+        L.eaas_expert_forward_noalloc.restype = i32
         L.eaas_segments_workspace_bytes.argtypes = [sp, i32]
         L.eaas_segments_workspace_bytes.restype = sz
         L.eaas_expert_forward_segments.argtypes = [sp, vp, vp, i32, vp, vp, vp, vp, i32, i32, vp,
@@ -258,6 +263,27 @@ def eaas_expert_forward(x: torch.Tensor, topk_ids: torch.Tensor, topk_weights: t
         raise ValueError("events must hold 5 entries")
     ev = (ctypes.c_void_p * 5)(*[e.cuda_event if e is not None else None for e in events])
     _check(lib().eaas_expert_forward_profiled(*args, ev), "eaas_expert_forward_profiled")
+
+
+def eaas_expert_forward_noalloc(x: torch.Tensor, topk_ids: torch.Tensor,
+                                topk_weights: torch.Tensor, w_gate_up: torch.Tensor,
+                                w_down: torch.Tensor, out: torch.Tensor, w_gate_up_scale=None,
+                                w_down_scale=None, routing: dict | None = None, stream=None,
+                                act8: bool = False) -> None:
+    """eaas_expert_forward on the library's own per-GPU scratch array: no
+    workspace argument, nothing allocated (shapes up to
+    EAAS_NOALLOC_SCRATCH_BYTES of workspace)."""
+    T, H = x.shape
+    E, twoI, _ = w_gate_up.shape
+    k = topk_ids.shape[1]
+    s = _shape(T, H, twoI // 2, E, k)
+    r = _routing(routing)
+    odt = EAAS_FP32 if out.dtype == torch.float32 else EAAS_BF16
+    _check(lib().eaas_expert_forward_noalloc(
+        ctypes.byref(s), _p(x), _p(topk_ids), _p(topk_weights), _p(w_gate_up),
+        _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8), _p(out), odt,
+        ctypes.byref(r) if r is not None else None, _stream(stream)),
+        "eaas_expert_forward_noalloc")
 
 
 def eaas_expert_forward_profiled(*args, events, **kwargs) -> None:
