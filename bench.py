@@ -432,6 +432,66 @@ def measure(name: str, steps: int, warmup: int):
     return res, d, dev, ms
 
 
+def scheduler_ablation(d: dict, dev: dict, steps: int, warmup: int) -> dict:
+    """The step with each build of the GEMM tile scheduler (§4.1
+    group-shrink ablation): the compacted active-expert list (the library),
+    the same parallel prefix scan over all E experts, and every workgroup
+    walking the E experts with one global read per expert.  Same inputs,
+    libraries interleaved twice; the outputs must agree bit for bit."""
+    import torch
+
+    from paper_2509_17863_amd import _build, eaas
+
+    T, H, I, E, k = d["T"], d["H"], d["I"], d["E"], d["k"]
+    act8 = bool(d.get("act8"))
+    wdt = (eaas.EAAS_FP8_E4M3_A8 if act8 else eaas.EAAS_FP8_E4M3) if d["wdtype"] == "fp8" \
+        else eaas.EAAS_BF16
+    variants = {"group_shrink": None, "scan_all": _build.variant_library("scan_all"),
+                "walk_all": _build.variant_library("walk_all")}
+    ws = eaas.alloc_workspace(T, H, I, E, k, wdt)
+    out = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
+    times = {n: [] for n in variants}
+    kern = {n: [] for n in variants}
+    same = {}
+    ref = None
+    try:
+        for _ in range(2):
+            for name, path in variants.items():
+                eaas.use_library(path)
+
+                def step(ev=None):
+                    args = (dev["x"], dev["topk_ids"], dev["topk_weights"], dev["w_gate_up"],
+                            dev["w_down"], out, ws, dev["w_gate_up_scale"], dev["w_down_scale"])
+                    if ev is None:
+                        eaas.eaas_expert_forward(*args, act8=act8)
+                    else:
+                        eaas.eaas_expert_forward_profiled(*args, events=ev, act8=act8)
+
+                ms, _ = time_graph(step, steps, warmup)
+                times[name].append(ms)
+                evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+                for ev in evs:
+                    step(ev)
+                torch.cuda.synchronize()
+                kern[name].append([float(np.mean([ev[a].elapsed_time(ev[a + 1]) for ev in evs]))
+                                   for a in range(4)])
+                bits = out.view(torch.int16).clone()
+                if ref is None:
+                    ref = bits
+                same[name] = same.get(name, True) and bool(torch.equal(bits, ref))
+    finally:
+        eaas.use_library(None)
+    base = float(np.median(times["group_shrink"]))
+    res = {}
+    for name in variants:
+        t = float(np.median(times[name]))
+        kmean = np.mean(np.array(kern[name]), axis=0)
+        res[name] = {"ms_per_step": round(t, 4), "vs_group_shrink": round(t / base, 4),
+                     "gate_up_ms": round(float(kmean[1]), 4), "down_ms": round(float(kmean[2]), 4),
+                     "runs_ms": [round(x, 4) for x in times[name]], "bitwise_equal": same[name]}
+    return res
+
+
 def decode_summary(r: dict) -> dict:
     """The decode-sized workload's figures for the headline line."""
     out = {"workload": r["config"]["workload"], "config": r["config"],
@@ -456,6 +516,10 @@ def main() -> int:
                     help="decode-sized workload timed in the same run for the HBM figures")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--scheduler-ablation", action="store_true",
+                    help="also time the step with the two other builds of the GEMM tile "
+                         "scheduler (all E experts scanned; all E walked with a global read "
+                         "each) on the headline workload")
     ap.add_argument("--server-slots", type=int, default=0,
                     help="also time the server step over this many client slots holding the "
                          "batch (flags set ready before every step)")
@@ -492,6 +556,8 @@ def main() -> int:
     if args.server_slots > 0:
         res["server_step"] = time_server(d, dev, args.server_slots, args.steps, args.warmup,
                                          ms_eager)
+    if args.scheduler_ablation:
+        res["scheduler_ablation"] = scheduler_ablation(d, dev, args.steps, args.warmup)
     res["clocks_mhz"] = {"before": clocks_before, "after": clocks_after}
     if not args.no_decode and args.decode_workload != args.workload:
         del dev

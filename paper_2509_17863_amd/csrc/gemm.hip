@@ -147,8 +147,97 @@ __device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t 
                :: "v"(voff), "s"(wave_uniform(base)), "s"(lds) : "memory");
 }
 
-// Group-shrink schedule: the active list and its M-tile prefix go to LDS once,
-// then this workgroup's tile is located.  Returns false for surplus groups.
+// Scheduler variant, fixed at build time (the default library is built with
+// 0; the other two are built beside it only to reproduce the §4.1 ablation):
+//   0  group-shrink: the compacted active-expert list of the routing is read
+//      into LDS and the M-tile prefix is scanned over it in parallel;
+//   1  the same parallel scan over all E experts, empty ones included;
+//   2  the scheduler the paper removes: every workgroup walks the E experts
+//      one at a time with one global read of the offsets per expert.
+// All three find the same tile for every workgroup id.
+#ifndef EAAS_SCHEDULER
+#define EAAS_SCHEDULER 0
+#endif
+
+// Workgroups are dispatched in id order and round-robin over the XCDs
+// (XCD = id mod 8).  The k-th workgroup of XCD x takes tile
+//   (k / 32) * 256 + x * 32 + k % 32,
+// so the 32 workgroups an XCD runs at once hold 32 consecutive tiles (they
+// share token and weight tiles in its L2) and the 256 running on the whole
+// GPU hold one window of 256 consecutive tiles, which keeps the weights the
+// XCDs re-read within the window in the shared MALL.  Tiles past the last
+// whole window keep their ids.
+__device__ __forceinline__ int xcd_window_remap(int bid, int total) {
+  constexpr int kChunk = 32;
+  constexpr int window = kNumXcd * kChunk;
+  if (bid >= (total / window) * window) return bid;
+  const int x = bid % kNumXcd, kk = bid / kNumXcd;
+  return (kk / kChunk) * window + x * kChunk + (kk % kChunk);
+}
+
+// Tile `local` of expert e (0 <= local < its M tiles x n_tiles_n).  Inside an
+// expert, tiles go in groups of kGroupM M-tiles: N-tile major, M-tile minor
+// within a group, so any 32 consecutive tiles (one XCD's workgroups at a
+// time) cover <= 8 M-tiles x >= 4 N-tiles and share operands.
+template <int BM>
+__device__ __forceinline__ void expert_tile(const GemmParams& p, int e, int mt, int local,
+                                            int n_tiles_n, Tile& t) {
+  const int g = local / (kGroupM * n_tiles_n);
+  const int gm = min(kGroupM, mt - g * kGroupM);
+  const int lg = local - g * kGroupM * n_tiles_n;
+  t.e = e;
+  t.tn = lg / gm;
+  const int tm = g * kGroupM + (lg - t.tn * gm);
+  const int beg = min(max(p.offsets[e], 0), p.R);
+  const int end = min(max(p.offsets[e + 1], beg), p.R);
+  t.r0 = beg + tm * BM;
+  t.rows_valid = min(BM, end - t.r0);
+}
+
+#if EAAS_SCHEDULER == 2
+// The walking scheduler: one thread walks all E experts twice (the tile
+// count, then the expert holding this workgroup's tile), one global read of
+// an expert's offsets per step.
+template <int BM, int BN, int NT>
+__device__ __forceinline__ bool locate_tile(const GemmParams& p, int* s_tp, int* s_exp,
+                                            int* s_wave, Tile& t) {
+  (void)s_tp; (void)s_exp;
+  const int n_tiles_n = p.N / BN;
+  auto m_tiles = [&](int e) {
+    const int beg = min(max(p.offsets[e], 0), p.R);
+    const int end = min(max(p.offsets[e + 1], beg), p.R);
+    return ceil_div(end - beg, BM);
+  };
+  if (threadIdx.x == 0) {
+    int all = 0;
+    for (int e = 0; e < p.E; ++e) all += m_tiles(e);
+    const int total = all * n_tiles_n;
+    s_wave[0] = total;
+    s_wave[1] = -1;
+    if ((int)blockIdx.x < total) {
+      const int tile = xcd_window_remap(blockIdx.x, total);
+      int before = 0;
+      for (int e = 0; e < p.E; ++e) {
+        const int mt = m_tiles(e);
+        if (tile < (before + mt) * n_tiles_n) {
+          s_wave[1] = e;
+          s_wave[2] = mt;
+          s_wave[3] = tile - before * n_tiles_n;
+          break;
+        }
+        before += mt;
+      }
+    }
+  }
+  __syncthreads();
+  if (s_wave[1] < 0) return false;
+  expert_tile<BM>(p, s_wave[1], s_wave[2], s_wave[3], n_tiles_n, t);
+  return true;
+}
+#else
+// Group-shrink schedule: the active list (scheduler 0; every expert for
+// scheduler 1) and its M-tile prefix go to LDS once, then this workgroup's
+// tile is located by a binary search.  Returns false for surplus groups.
 template <int BM, int BN, int NT>
 __device__ __forceinline__ bool locate_tile(const GemmParams& p, int* s_tp, int* s_exp,
                                             int* s_wave, Tile& t) {
@@ -156,7 +245,7 @@ __device__ __forceinline__ bool locate_tile(const GemmParams& p, int* s_tp, int*
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
   // routing arrays may come from the caller: clamp every index taken from them
-  const int n_active = min(max(p.active[0], 0), p.E);
+  const int n_active = EAAS_SCHEDULER == 1 ? p.E : min(max(p.active[0], 0), p.E);
   constexpr int PER = (kMaxExperts + NT) / NT;  // entries per thread (plus the end)
   int loc[PER];
   int sum = 0;
@@ -165,7 +254,7 @@ __device__ __forceinline__ bool locate_tile(const GemmParams& p, int* s_tp, int*
     const int a = tid * PER + i;
     int c = 0;
     if (a < n_active) {
-      const int e = min(max(p.active[1 + a], 0), p.E - 1);
+      const int e = EAAS_SCHEDULER == 1 ? a : min(max(p.active[1 + a], 0), p.E - 1);
       s_exp[a] = e;
       const int beg = min(max(p.offsets[e], 0), p.R);
       const int end = min(max(p.offsets[e + 1], beg), p.R);
@@ -197,46 +286,19 @@ __device__ __forceinline__ bool locate_tile(const GemmParams& p, int* s_tp, int*
   const int total = s_tp[n_active] * n_tiles_n;
   const int bid = blockIdx.x;
   if (bid >= total) return false;
-  // Workgroups are dispatched in id order and round-robin over the XCDs
-  // (XCD = id mod 8).  The k-th workgroup of XCD x takes tile
-  //   (k / 32) * 256 + x * 32 + k % 32,
-  // so the 32 workgroups an XCD runs at once hold 32 consecutive tiles (they
-  // share token and weight tiles in its L2) and the 256 running on the whole
-  // GPU hold one window of 256 consecutive tiles, which keeps the weights the
-  // XCDs re-read within the window in the shared MALL.  Tiles past the last
-  // whole window keep their ids.
-  int tile = bid;
-  {
-    constexpr int kChunk = 32;
-    const int window = kNumXcd * kChunk;
-    if (bid < (total / window) * window) {
-      const int x = bid % kNumXcd, kk = bid / kNumXcd;
-      tile = (kk / kChunk) * window + x * kChunk + (kk % kChunk);
-    }
-  }
+  const int tile = xcd_window_remap(bid, total);
+  // the last slot whose prefix is <= tile (empty experts of scheduler 1 share
+  // their successor's prefix and are passed over)
   int lo = 0, hi = n_active - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
     if (s_tp[mid] * n_tiles_n <= tile) lo = mid; else hi = mid - 1;
   }
-  const int e = s_exp[lo];
-  const int mt = s_tp[lo + 1] - s_tp[lo];
-  const int local = tile - s_tp[lo] * n_tiles_n;
-  // inside an expert, tiles go in groups of kGroupM M-tiles: N-tile major,
-  // M-tile minor within a group, so any 32 consecutive tiles (one XCD's
-  // workgroups at a time) cover <= 8 M-tiles x >= 4 N-tiles and share operands
-  const int g = local / (kGroupM * n_tiles_n);
-  const int gm = min(kGroupM, mt - g * kGroupM);
-  const int lg = local - g * kGroupM * n_tiles_n;
-  t.e = e;
-  t.tn = lg / gm;
-  const int tm = g * kGroupM + (lg - t.tn * gm);
-  const int beg = min(max(p.offsets[e], 0), p.R);
-  const int end = min(max(p.offsets[e + 1], beg), p.R);
-  t.r0 = beg + tm * BM;
-  t.rows_valid = min(BM, end - t.r0);
+  expert_tile<BM>(p, s_exp[lo], s_tp[lo + 1] - s_tp[lo], tile - s_tp[lo] * n_tiles_n, n_tiles_n,
+                  t);
   return true;
 }
+#endif
 
 // Weight row (of the expert's [N, K] matrix) held by LDS row j of an N tile.
 template <bool GATEUP, int BN>

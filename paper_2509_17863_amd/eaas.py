@@ -24,6 +24,7 @@ __all__ = [
     "EAAS_WS_H", "EAAS_WS_HQ", "EAAS_WS_HS", "EAAS_WS_XQ", "EAAS_WS_XS", "EAAS_WS_STAGE",
     "eaas_workspace_bytes_for", "EAAS_ENTRY_ROUTE_PERMUTE", "EAAS_ENTRY_FFN_GROUPED",
     "EAAS_ENTRY_FORWARD", "eaas_expert_forward_noalloc", "EAAS_NOALLOC_SCRATCH_BYTES",
+    "use_library",
 ]
 
 EAAS_OK = 0
@@ -39,7 +40,8 @@ EXPORTED = ("eaas_workspace_bytes", "eaas_route_permute", "eaas_expert_ffn_group
             "eaas_quantize_rows_fp8", "eaas_workspace_region", "eaas_workspace_bytes_for",
             "eaas_expert_forward_noalloc")
 
-_LIB_PATH = Path(__file__).resolve().parent / "libeaas.so"
+_DEFAULT_LIB = Path(__file__).resolve().parent / "libeaas.so"
+_LIB_PATH = _DEFAULT_LIB
 _lib = None
 
 
@@ -64,50 +66,63 @@ def library_path() -> Path:
     return _LIB_PATH
 
 
+def _bind(L: ctypes.CDLL) -> ctypes.CDLL:
+    vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+    sp, rp = ctypes.POINTER(_Shape), ctypes.POINTER(_Routing)
+    L.eaas_workspace_bytes.argtypes = [sp, i32]
+    L.eaas_workspace_bytes.restype = sz
+    L.eaas_workspace_bytes_for.argtypes = [sp, i32, i32]
+    L.eaas_workspace_bytes_for.restype = sz
+    L.eaas_route_permute.argtypes = [sp, vp, rp, vp, sz, vp]
+    L.eaas_route_permute.restype = i32
+    L.eaas_expert_ffn_grouped.argtypes = [sp, vp, rp, vp, vp, vp, vp, i32, vp, vp, sz, vp]
+    L.eaas_expert_ffn_grouped.restype = i32
+    L.eaas_unpermute_combine.argtypes = [sp, vp, rp, vp, vp, i32, vp]
+    L.eaas_unpermute_combine.restype = i32
+    L.eaas_expert_forward.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, rp, vp, sz, vp]
+    L.eaas_expert_forward.restype = i32
+    L.eaas_expert_forward_profiled.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32,
+                                               rp, vp, sz, vp, vp]
+    L.eaas_expert_forward_profiled.restype = i32
+    L.eaas_expert_forward_noalloc.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32,
+                                              rp, vp]
+    L.eaas_expert_forward_noalloc.restype = i32
+    L.eaas_segments_workspace_bytes.argtypes = [sp, i32]
+    L.eaas_segments_workspace_bytes.restype = sz
+    L.eaas_expert_forward_segments.argtypes = [sp, vp, vp, i32, vp, vp, vp, vp, i32, i32, vp,
+                                               sz, vp]
+    L.eaas_expert_forward_segments.restype = i32
+    L.eaas_server_workspace_bytes.argtypes = [sp, i32, i32]
+    L.eaas_server_workspace_bytes.restype = sz
+    L.eaas_server_step.argtypes = [sp, vp, i32, vp, i32, i32, vp, sz, vp]
+    L.eaas_server_step.restype = i32
+    L.eaas_quantize_rows_fp8.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, vp, vp, vp]
+    L.eaas_quantize_rows_fp8.restype = i32
+    L.eaas_workspace_region.argtypes = [sp, i32, i32, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    L.eaas_workspace_region.restype = i32
+    L.eaas_status_string.argtypes = [i32]
+    L.eaas_status_string.restype = ctypes.c_char_p
+    return L
+
+
 def lib() -> ctypes.CDLL:
     """Load libeaas.so (raises if it has not been built)."""
     global _lib
     if _lib is None:
         if not _LIB_PATH.exists():
             raise RuntimeError(f"{_LIB_PATH} is missing: build it with __graft_entry__.build()")
-        L = ctypes.CDLL(str(_LIB_PATH))
-        vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
-        sp, rp = ctypes.POINTER(_Shape), ctypes.POINTER(_Routing)
-        L.eaas_workspace_bytes.argtypes = [sp, i32]
-        L.eaas_workspace_bytes.restype = sz
-        L.eaas_workspace_bytes_for.argtypes = [sp, i32, i32]
-        L.eaas_workspace_bytes_for.restype = sz
-        L.eaas_route_permute.argtypes = [sp, vp, rp, vp, sz, vp]
-        L.eaas_route_permute.restype = i32
-        L.eaas_expert_ffn_grouped.argtypes = [sp, vp, rp, vp, vp, vp, vp, i32, vp, vp, sz, vp]
-        L.eaas_expert_ffn_grouped.restype = i32
-        L.eaas_unpermute_combine.argtypes = [sp, vp, rp, vp, vp, i32, vp]
-        L.eaas_unpermute_combine.restype = i32
-        L.eaas_expert_forward.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, rp, vp, sz, vp]
-        L.eaas_expert_forward.restype = i32
-        L.eaas_expert_forward_profiled.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32,
-                                                   rp, vp, sz, vp, vp]
-        L.eaas_expert_forward_profiled.restype = i32
-        L.eaas_expert_forward_noalloc.argtypes = [sp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32,
-                                                  rp, vp]
-        L.eaas_expert_forward_noalloc.restype = i32
-        L.eaas_segments_workspace_bytes.argtypes = [sp, i32]
-        L.eaas_segments_workspace_bytes.restype = sz
-        L.eaas_expert_forward_segments.argtypes = [sp, vp, vp, i32, vp, vp, vp, vp, i32, i32, vp,
-                                                   sz, vp]
-        L.eaas_expert_forward_segments.restype = i32
-        L.eaas_server_workspace_bytes.argtypes = [sp, i32, i32]
-        L.eaas_server_workspace_bytes.restype = sz
-        L.eaas_server_step.argtypes = [sp, vp, i32, vp, i32, i32, vp, sz, vp]
-        L.eaas_server_step.restype = i32
-        L.eaas_quantize_rows_fp8.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, vp, vp, vp]
-        L.eaas_quantize_rows_fp8.restype = i32
-        L.eaas_workspace_region.argtypes = [sp, i32, i32, ctypes.POINTER(sz), ctypes.POINTER(sz)]
-        L.eaas_workspace_region.restype = i32
-        L.eaas_status_string.argtypes = [i32]
-        L.eaas_status_string.restype = ctypes.c_char_p
-        _lib = L
+        _lib = _bind(ctypes.CDLL(str(_LIB_PATH)))
     return _lib
+
+
+def use_library(path) -> ctypes.CDLL:
+    """Route every later call of this module through the library at `path`
+    (a build of the same sources, e.g. a scheduler variant for the
+    group-shrink ablation); None returns to libeaas.so."""
+    global _lib, _LIB_PATH
+    _LIB_PATH = Path(path) if path is not None else _DEFAULT_LIB
+    _lib = None
+    return lib()
 
 
 def eaas_status_string(status: int) -> str:

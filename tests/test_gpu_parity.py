@@ -542,3 +542,26 @@ def test_forward_k_above_E(gpu):
     torch.cuda.synchronize()
     assert_routing_equal({key: v.cpu().numpy() for key, v in r.items()}, ref["routing"], T * k, E)
     check_close(out.cpu().numpy(), ref["out"], "k=8 > E=3")
+
+
+@pytest.mark.parametrize("shape", [(300, 256, 256, 1024, 8, 83, None, "bf16"),
+                                   (700, 512, 384, 40, 4, 84, 1.5, "bf16"),
+                                   (200, 512, 256, 12, 4, 85, 1.2, "fp8")])
+def test_scheduler_builds_agree_bitwise(gpu, shape):
+    """The two other builds of the GEMM tile scheduler (all E experts
+    scanned; every workgroup walking the E experts) find the same tiles:
+    bitwise the same output as the library (group-shrink ablation builds)."""
+    from paper_2509_17863_amd import _build
+
+    T, H, I, E, k, seed, zipf, wdtype = shape
+    d = synth.make_inputs(T, H, I, E, k, seed, zipf=zipf, wdtype=wdtype)
+    dev = to_device(d)
+    say("scheduler builds", shape)
+    ref = forward(dev, k).cpu().numpy()
+    try:
+        for name in _build.SCHEDULER_VARIANTS:
+            eaas.use_library(_build.variant_library(name))
+            got = forward(dev, k).cpu().numpy()
+            assert np.array_equal(got.view(np.uint32), ref.view(np.uint32)), name
+    finally:
+        eaas.use_library(None)
