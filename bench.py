@@ -238,7 +238,8 @@ def gpu_clocks() -> dict | None:
     return None
 
 
-def time_segments(d: dict, dev: dict, clients: int, steps: int, warmup: int, ms_single: float):
+def time_segments(d: dict, dev: dict, clients: int, steps: int, warmup: int, ms_single: float,
+                  tiled: bool = False):
     """The same batch as `clients` requests in separate buffers, through
     eaas_expert_forward_segments (counts on the device, capacity T)."""
     import torch
@@ -257,13 +258,15 @@ def time_segments(d: dict, dev: dict, clients: int, steps: int, warmup: int, ms_
     act8 = bool(d.get("act8"))
     wdt = (eaas.EAAS_FP8_E4M3_A8 if act8 else eaas.EAAS_FP8_E4M3) if d["wdtype"] == "fp8" \
         else eaas.EAAS_BF16
+    if tiled:
+        wdt = eaas.EAAS_FP8_E4M3_TILED
     ws = eaas.alloc_segments_workspace(T, H, I, E, k, wdt)
 
     def step():
         eaas.eaas_expert_forward_segments(table, counts, clients, T, k, dev["w_gate_up"],
                                           dev["w_down"], ws, eaas.EAAS_BF16,
                                           dev["w_gate_up_scale"], dev["w_down_scale"],
-                                          act8=act8)
+                                          act8=act8, tiled=tiled)
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
@@ -278,7 +281,8 @@ def time_segments(d: dict, dev: dict, clients: int, steps: int, warmup: int, ms_
             "vs_single_batch": round(ms / ms_single, 4)}
 
 
-def time_server(d: dict, dev: dict, n_slots: int, steps: int, warmup: int, ms_single: float):
+def time_server(d: dict, dev: dict, n_slots: int, steps: int, warmup: int, ms_single: float,
+                tiled: bool = False):
     """The batch spread over `n_slots` client slots of one layer, served by
     eaas_server_step.  The step writes its results over the hidden states, so
     before every step the clients' requests are posted again: the hidden
@@ -302,6 +306,8 @@ def time_server(d: dict, dev: dict, n_slots: int, steps: int, warmup: int, ms_si
     act8 = bool(d.get("act8"))
     wdt = (eaas.EAAS_FP8_E4M3_A8 if act8 else eaas.EAAS_FP8_E4M3) if d["wdtype"] == "fp8" \
         else eaas.EAAS_BF16
+    if tiled:
+        wdt = eaas.EAAS_FP8_E4M3_TILED
     ws = eaas.alloc_server_workspace(T, H, I, E, k, 1, wdt)
 
     def step():
@@ -324,7 +330,7 @@ def time_server(d: dict, dev: dict, n_slots: int, steps: int, warmup: int, ms_si
             "vs_single_batch": round(ms / ms_single, 4)}
 
 
-def measure(name: str, steps: int, warmup: int):
+def measure(name: str, steps: int, warmup: int, tiled_fp8: bool = True):
     """Time eaas_expert_forward on one workload: a graph-replayed pass for the
     step time and an eager pass with events between the kernels."""
     import torch
@@ -339,6 +345,16 @@ def measure(name: str, steps: int, warmup: int):
     act8 = bool(d.get("act8"))
     wdt = (eaas.EAAS_FP8_E4M3_A8 if act8 else eaas.EAAS_FP8_E4M3) if d["wdtype"] == "fp8" \
         else eaas.EAAS_BF16
+    # fp8 weights (bf16 activations) are rearranged once, as a server would
+    # when it loads them, into the tiled layout the fp8 GEMMs stream
+    tiled = tiled_fp8 and wdt == eaas.EAAS_FP8_E4M3 and H % 256 == 0
+    if tiled:
+        for key, which in (("w_gate_up", eaas.EAAS_GATE_UP), ("w_down", eaas.EAAS_DOWN)):
+            t = torch.empty_like(dev[key])
+            eaas.eaas_tile_weights_fp8(dev[key], which, H, I, t)
+            dev[key] = t
+        torch.cuda.synchronize()
+        wdt = eaas.EAAS_FP8_E4M3_TILED
     ws = eaas.alloc_workspace(T, H, I, E, k, wdt)
     out = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
     counts = np.bincount(d["topk_ids"].ravel()[d["topk_ids"].ravel() >= 0], minlength=E)
@@ -351,12 +367,13 @@ def measure(name: str, steps: int, warmup: int):
         if ev is None:
             eaas.eaas_expert_forward(dev["x"], dev["topk_ids"], dev["topk_weights"],
                                      dev["w_gate_up"], dev["w_down"], out, ws,
-                                     dev["w_gate_up_scale"], dev["w_down_scale"], act8=act8)
+                                     dev["w_gate_up_scale"], dev["w_down_scale"], act8=act8,
+                                     tiled=tiled)
         else:
             eaas.eaas_expert_forward_profiled(dev["x"], dev["topk_ids"], dev["topk_weights"],
                                               dev["w_gate_up"], dev["w_down"], out, ws,
                                               dev["w_gate_up_scale"], dev["w_down_scale"],
-                                              events=ev, act8=act8)
+                                              events=ev, act8=act8, tiled=tiled)
 
     for ev in evs:  # create the events before the timed region
         for e in ev:
@@ -400,7 +417,7 @@ def measure(name: str, steps: int, warmup: int):
     roof["algorithmic_bytes"] = int(alg["gu_bytes"])
     roof["algorithmic_flops"] = alg["gu_flops"]
     roof["launch_ms"] = round(t_gu, 4)
-    roof["kernel"] = gate_up_kernel_name(d)
+    roof["kernel"] = gate_up_kernel_name(d) + (", tiled weights" if tiled else "")
     res = {
         "value": round(T / (ms_graph * 1e-3), 1),
         "ms_per_step": round(ms_graph, 4),
@@ -410,6 +427,7 @@ def measure(name: str, steps: int, warmup: int):
         "dtype": "fp8e4m3" if act8 else "bf16",
         "config": {"workload": name, "T": T, "H": H, "I": I, "E": E, "k": k,
                    "weights": d["wdtype"], "activations": "fp8e4m3" if act8 else "bf16",
+                   "weight_layout": "tiled" if tiled else "row_major",
                    "seed": wl.seed, "zipf": wl.zipf,
                    "active_experts": int((counts > 0).sum()), "parallelism": "none (1 GPU)"},
         "step_tflops": round(alg["flops"] / (ms_graph * 1e-3) / 1e12, 1),
@@ -429,10 +447,11 @@ def measure(name: str, steps: int, warmup: int):
         step_gbs = (alg["gu_bytes"] + alg["dn_bytes"]) / (ms_graph * 1e-3) / 1e9
         res["step_hbm_gbs"] = round(step_gbs, 1)
         res["step_hbm_frac"] = round(step_gbs / PEAK_HBM_GBS, 4)
+    res["_tiled"] = tiled
     return res, d, dev, ms
 
 
-def scheduler_ablation(d: dict, dev: dict, steps: int, warmup: int) -> dict:
+def scheduler_ablation(d: dict, dev: dict, steps: int, warmup: int, tiled: bool = False) -> dict:
     """The step with each build of the GEMM tile scheduler (§4.1
     group-shrink ablation): the compacted active-expert list (the library),
     the same parallel prefix scan over all E experts, and every workgroup
@@ -446,6 +465,8 @@ def scheduler_ablation(d: dict, dev: dict, steps: int, warmup: int) -> dict:
     act8 = bool(d.get("act8"))
     wdt = (eaas.EAAS_FP8_E4M3_A8 if act8 else eaas.EAAS_FP8_E4M3) if d["wdtype"] == "fp8" \
         else eaas.EAAS_BF16
+    if tiled:
+        wdt = eaas.EAAS_FP8_E4M3_TILED
     variants = {"group_shrink": None, "scan_all": _build.variant_library("scan_all"),
                 "walk_all": _build.variant_library("walk_all")}
     ws = eaas.alloc_workspace(T, H, I, E, k, wdt)
@@ -463,9 +484,10 @@ def scheduler_ablation(d: dict, dev: dict, steps: int, warmup: int) -> dict:
                     args = (dev["x"], dev["topk_ids"], dev["topk_weights"], dev["w_gate_up"],
                             dev["w_down"], out, ws, dev["w_gate_up_scale"], dev["w_down_scale"])
                     if ev is None:
-                        eaas.eaas_expert_forward(*args, act8=act8)
+                        eaas.eaas_expert_forward(*args, act8=act8, tiled=tiled)
                     else:
-                        eaas.eaas_expert_forward_profiled(*args, events=ev, act8=act8)
+                        eaas.eaas_expert_forward_profiled(*args, events=ev, act8=act8,
+                                                          tiled=tiled)
 
                 ms, _ = time_graph(step, steps, warmup)
                 times[name].append(ms)
@@ -515,6 +537,9 @@ def main() -> int:
     ap.add_argument("--decode-workload", default="dsv3_decode",
                     help="decode-sized workload timed in the same run for the HBM figures")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--row-major-fp8", action="store_true",
+                    help="time fp8 weights in their row-major [E,N,K] layout instead of the "
+                         "tiled layout of eaas_tile_weights_fp8")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--scheduler-ablation", action="store_true",
                     help="also time the step with the two other builds of the GEMM tile "
@@ -537,7 +562,8 @@ def main() -> int:
 
     assert torch.cuda.is_available(), "no GPU"
     clocks_before = gpu_clocks()
-    r, d, dev, ms_eager = measure(args.workload, args.steps, args.warmup)
+    r, d, dev, ms_eager = measure(args.workload, args.steps, args.warmup,
+                                  tiled_fp8=not args.row_major_fp8)
     clocks_after = gpu_clocks()
     res = {
         "metric": "expert-FFN tokens/s",
@@ -550,19 +576,23 @@ def main() -> int:
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "data": "synthetic",
     }
+    tiled = r.pop("_tiled", False)
     res.update({key: v for key, v in r.items() if key not in res})
     if args.clients > 0:
-        res["segments"] = time_segments(d, dev, args.clients, args.steps, args.warmup, ms_eager)
+        res["segments"] = time_segments(d, dev, args.clients, args.steps, args.warmup, ms_eager,
+                                        tiled)
     if args.server_slots > 0:
         res["server_step"] = time_server(d, dev, args.server_slots, args.steps, args.warmup,
-                                         ms_eager)
+                                         ms_eager, tiled)
     if args.scheduler_ablation:
-        res["scheduler_ablation"] = scheduler_ablation(d, dev, args.steps, args.warmup)
+        res["scheduler_ablation"] = scheduler_ablation(d, dev, args.steps, args.warmup, tiled)
     res["clocks_mhz"] = {"before": clocks_before, "after": clocks_after}
     if not args.no_decode and args.decode_workload != args.workload:
         del dev
         torch.cuda.empty_cache()
-        rd, _, _, _ = measure(args.decode_workload, max(args.steps, 200), args.warmup)
+        rd, _, _, _ = measure(args.decode_workload, max(args.steps, 200), args.warmup,
+                              tiled_fp8=not args.row_major_fp8)
+        rd.pop("_tiled", None)
         res["decode"] = decode_summary(rd)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(d)

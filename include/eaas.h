@@ -88,7 +88,13 @@ enum eaas_dtype {
    * block-scaled fp8 GEMM of the grouped-GEMM engine named in §4.1).  Needs
    * H a multiple of 256.  Accepted by every entry point that takes a
    * weight dtype. */
-  EAAS_FP8_E4M3_A8 = 3
+  EAAS_FP8_E4M3_A8 = 3,
+  /* As a weight dtype: the fp8 e4m3fn weights of EAAS_FP8_E4M3 (same values,
+   * same scales, same results bit for bit) stored in the tiled layout that
+   * eaas_tile_weights_fp8 writes, which the decode-sized fp8 GEMMs stream as
+   * contiguous blocks instead of rows K bytes apart.  Needs H a multiple of
+   * 256.  Accepted by every entry point that takes a weight dtype. */
+  EAAS_FP8_E4M3_TILED = 4
 };
 
 /*
@@ -160,6 +166,27 @@ int eaas_workspace_region(const eaas_shape *s, int w_dtype, int region, size_t *
  * misaligned pointer, rows < 0, K <= 0), UNSUPPORTED (K % 128, size), HIP. */
 int eaas_quantize_rows_fp8(const void *x, int64_t rows, int32_t K, void *q, float *s,
                            void *stream);
+
+/* The fp8 weight layout of EAAS_FP8_E4M3_TILED (weights stay resident on a
+ * server, so they are rearranged once, when loaded).
+ *   which    EAAS_GATE_UP: w is W_gate_up [E,2I,H] (N = 2I rows, K = H);
+ *            EAAS_DOWN:    w is W_down    [E,H,I] (N = H rows, K = I)
+ *   w        e4m3fn codes [E,N,K], row-major (device, read)
+ *   w_tiled  E*N*K bytes (device, written), the same codes reordered: with
+ *            BN = 512 for a gate/up matrix whose 2I is a multiple of 512 and
+ *            256 otherwise, for expert e, N tile tn < N/BN, K tile kt < K/64,
+ *            j < BN and b < 64,
+ *              w_tiled[((e*(N/BN) + tn)*(K/64) + kt)*BN*64 + j*64 + b]
+ *                = w[e][row(tn, j)][64*kt + b],
+ *            row(tn, j) = tn*BN + j for W_down; for W_gate_up the tile's BN/2
+ *            gate rows come first: row(tn, j) = tn*BN/2 + j for j < BN/2,
+ *            I + tn*BN/2 + j - BN/2 otherwise.
+ * The block scales are not moved.  s->T is not used (any valid value).
+ * Errors: INVALID_ARG (unknown `which`, null, misaligned or overlapping
+ * pointers), UNSUPPORTED (the shape, or H not a multiple of 256), HIP. */
+enum eaas_matrix { EAAS_GATE_UP = 0, EAAS_DOWN = 1 };
+int eaas_tile_weights_fp8(const eaas_shape *s, int which, const void *w, void *w_tiled,
+                          void *stream);
 
 /* Token reorganisation + group-shrink (§3.3 Fig. 5, §4.1).
  *   topk_ids [T,k] int32   expert id per slot (payload `expert_id`, §3.2)

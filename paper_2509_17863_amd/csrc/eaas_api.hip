@@ -82,21 +82,30 @@ bool routing_ok(const eaas_routing* r) {
 bool weights_ok(const void* wgu, const float* sgu, const void* wd, const float* sd, int w_dtype) {
   if (!wgu || !wd || !aligned16(wgu) || !aligned16(wd)) return false;
   if (w_dtype == EAAS_BF16) return true;
-  if (w_dtype == EAAS_FP8_E4M3 || w_dtype == EAAS_FP8_E4M3_A8) return sgu && sd;
+  if (w_dtype == EAAS_FP8_E4M3 || w_dtype == EAAS_FP8_E4M3_A8 || w_dtype == EAAS_FP8_E4M3_TILED)
+    return sgu && sd;
   return false;
 }
 
-// Shape limits of a weight dtype beyond check_shape (fp8 activations: the
-// down projection's N = H in 256-wide tiles).
+// Shape limits of a weight dtype beyond check_shape (fp8 activations and
+// tiled fp8 weights: the down projection's N = H in 256-wide tiles).
 int check_dtype_shape(const eaas_shape* s, int w_dtype) {
-  if (w_dtype == EAAS_FP8_E4M3_A8 && s->H % 256) return EAAS_ERR_UNSUPPORTED;
+  if ((w_dtype == EAAS_FP8_E4M3_A8 || w_dtype == EAAS_FP8_E4M3_TILED) && s->H % 256)
+    return EAAS_ERR_UNSUPPORTED;
   return EAAS_OK;
+}
+
+bool known_wdtype(int w_dtype) {
+  return w_dtype == EAAS_BF16 || w_dtype == EAAS_FP8_E4M3 || w_dtype == EAAS_FP8_E4M3_A8 ||
+         w_dtype == EAAS_FP8_E4M3_TILED;
 }
 
 // FfnArgs members of the weight dtype (h and y are set by the caller).
 void set_dtype_args(FfnArgs& a, int w_dtype, char* base, const WsLayout& L) {
-  a.fp8 = w_dtype == EAAS_FP8_E4M3 || w_dtype == EAAS_FP8_E4M3_A8;
+  a.fp8 = w_dtype == EAAS_FP8_E4M3 || w_dtype == EAAS_FP8_E4M3_A8 ||
+          w_dtype == EAAS_FP8_E4M3_TILED;
   a.act8 = w_dtype == EAAS_FP8_E4M3_A8;
+  a.tiled = w_dtype == EAAS_FP8_E4M3_TILED;
   if (a.act8) {
     a.xq = reinterpret_cast<const uint8_t*>(base + L.xq);
     a.xs = reinterpret_cast<const float*>(base + L.xs);
@@ -130,7 +139,7 @@ extern "C" {
 
 size_t eaas_workspace_bytes(const eaas_shape* s, int w_dtype) {
   if (check_shape(s) != EAAS_OK) return 0;
-  if (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3 && w_dtype != EAAS_FP8_E4M3_A8) return 0;
+  if (!known_wdtype(w_dtype)) return 0;
   if (check_dtype_shape(s, w_dtype) != EAAS_OK) return 0;
   return layout(*s, w_dtype).total;
 }
@@ -174,6 +183,24 @@ int eaas_workspace_region(const eaas_shape* s, int w_dtype, int region, size_t* 
     default:
       return EAAS_ERR_INVALID_ARG;
   }
+}
+
+int eaas_tile_weights_fp8(const eaas_shape* s, int which, const void* w, void* w_tiled,
+                          void* stream) {
+  int st = check_shape(s);
+  if (st != EAAS_OK) return st;
+  if (which != EAAS_GATE_UP && which != EAAS_DOWN) return EAAS_ERR_INVALID_ARG;
+  if ((st = check_dtype_shape(s, EAAS_FP8_E4M3_TILED)) != EAAS_OK) return st;
+  if (!w || !w_tiled || !aligned16(w) || !aligned16(w_tiled)) return EAAS_ERR_INVALID_ARG;
+  const int N = which == EAAS_GATE_UP ? 2 * s->I : s->H;
+  const int K = which == EAAS_GATE_UP ? s->H : s->I;
+  const size_t bytes = (size_t)s->E * N * K;
+  const uintptr_t a = (uintptr_t)w, b = (uintptr_t)w_tiled;
+  if (a < b + bytes && b < a + bytes) return EAAS_ERR_INVALID_ARG;  // no overlap, no in-place
+  return hip_status(launch_tile_weights_fp8(static_cast<const uint8_t*>(w),
+                                            static_cast<uint8_t*>(w_tiled), s->E, N, K,
+                                            which == EAAS_GATE_UP ? s->I : 0,
+                                            reinterpret_cast<hipStream_t>(stream)));
 }
 
 int eaas_quantize_rows_fp8(const void* x, int64_t rows, int32_t K, void* q, float* s,
@@ -437,7 +464,7 @@ int eaas_server_step(const eaas_shape* s, const eaas_slot* slots, int n_slots,
   if ((st = check_dtype_shape(&g, w_dtype)) != EAAS_OK) return st;
   if (n_slots == 0) return EAAS_OK;
   if (!slots || !layers ||
-      (w_dtype != EAAS_BF16 && w_dtype != EAAS_FP8_E4M3 && w_dtype != EAAS_FP8_E4M3_A8))
+      !known_wdtype(w_dtype))
     return EAAS_ERR_INVALID_ARG;
   const WsLayout L = layout(g, w_dtype);
   const SlotLayout SL = slot_layout(L.seg_total);

@@ -48,6 +48,7 @@
 // window of 256 consecutive tiles (the MALL sees the re-reads across XCDs).
 // The grid is sized for the worst case from R and E alone (no host
 // readback); surplus workgroups exit after the prologue.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -93,6 +94,9 @@ struct GemmParams {
   const float* a_scale;
   uint8_t* hq;
   float* hs;
+  // fp8 weights in the tiled layout of tile_weights_fp8 (the ring kernels'
+  // weight stages stored contiguously) instead of [E, N, K] row-major
+  bool tiled;
 };
 
 // Weights of group e ([N, K], bf16 or fp8 bytes of esz each).
@@ -478,7 +482,8 @@ __device__ __forceinline__ int swz(int row) {
 template <int A_INST, int B_INST>
 struct DmaSrc {
   const char* a;             // A base (bytes); K tile kt starts kt*BK*2 bytes further
-  const char* b;             // B base of the expert (bytes)
+  const char* b;             // B base of the tile (bytes)
+  uint32_t b_kstride;        // bytes from one B stage's K position to the next
   uint32_t a_off[A_INST];    // per-lane byte offsets of this lane's DMA rows
   uint32_t b_off[B_INST];
   uint32_t lds;              // LDS byte address of stage 0
@@ -551,7 +556,7 @@ struct DmaLoop {
               s.lds + (ka % SA) * A_BYTES + a_inst(s.wave, q) * RPI * RB);
     } else {
       if (kb >= 0 && kb < nb)
-        dma16(s.b + kb * BRB, s.b_off[q - A_INST],
+        dma16(s.b + (size_t)kb * s.b_kstride, s.b_off[q - A_INST],
               s.lds + B_BASE + (kb % SB) * B_BYTES + b_inst(s.wave, q - A_INST) * BRPI * BRB);
     }
   }
@@ -792,6 +797,11 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   src.wave = wave;
   src.a = reinterpret_cast<const char*>(p.a);
   src.b = reinterpret_cast<const char*>(group_weights(p, t.e, FP8 ? 1 : 2));
+  // tiled fp8 weights: N tile tn's stages are BN rows x BRB bytes, stored one
+  // after the other along K (see tile_weights_fp8)
+  const bool tiled = FP8 && BSPAN == 1 && p.tiled;
+  src.b_kstride = tiled ? (uint32_t)(BN * BRB) : (uint32_t)BRB;
+  if (tiled) src.b += (size_t)t.tn * (p.K / BK) * BN * BRB;
   {
     const int drow = lane / CH;
     const int dpc = lane % CH;
@@ -810,8 +820,9 @@ void grouped_gemm_dma_kernel(GemmParams p) {
     for (int i = 0; i < Full::B_INST; ++i) {
       const int j = Full::b_inst(wave, i) * BRPI + drow;
       const int chunk = dpc ^ swz<BRB>(j);
-      src.b_off[i] = (uint32_t)weight_row<GATEUP, BN>(p, t.tn, j) * (uint32_t)p.K * (FP8 ? 1u : 2u) +
-                     (uint32_t)chunk * 16u;
+      src.b_off[i] = tiled ? (uint32_t)(j * BRB + chunk * 16)
+                           : (uint32_t)weight_row<GATEUP, BN>(p, t.tn, j) * (uint32_t)p.K *
+                                 (FP8 ? 1u : 2u) + (uint32_t)chunk * 16u;
     }
   }
 
@@ -1665,6 +1676,41 @@ hipError_t launch_w8a8(const GemmParams& p, int R, int E, bool small_m, hipStrea
                  : launch_w8a8_mb<KIND, 6>(p, R, E, stream);
 }
 
+// N-tile width of the fp8-weight ring kernels (launch_kind below): 512 for
+// a gate/up matrix whose 2I rows are a multiple of 512, else 256.
+inline int fp8_tile_width(bool gateup, int N) { return gateup && N % 512 == 0 ? 512 : 256; }
+
+// Tiled fp8 weights: for expert e, N tile tn (BN rows) and K tile kt (64
+// bytes), the BN row slices the ring kernel loads into one weight stage are
+// stored contiguously, in the stage's row order (gate/up: the tile's BN/2
+// gate rows, then the matching up rows):
+//   tiled[((e * N/BN + tn) * K/64 + kt) * BN * 64 + j * 64 + b]
+//     = w[e][row(tn, j)][kt * 64 + b]
+// One thread per 16-byte chunk of the output.
+__global__ __launch_bounds__(256) void tile_weights_fp8_kernel(const uint8_t* __restrict__ w,
+                                                               uint8_t* __restrict__ out, int E,
+                                                               int N, int K, int I, int BN) {
+  const long long chunks = (long long)E * N * K / 16;
+  for (long long c = (long long)blockIdx.x * blockDim.x + threadIdx.x; c < chunks;
+       c += (long long)gridDim.x * blockDim.x) {
+    const long long byte = c * 16;
+    const int b = (int)(byte % 64);
+    const long long slice = byte / 64;          // (e, tn, kt, j)
+    const int j = (int)(slice % BN);
+    const long long tk = slice / BN;             // (e, tn, kt)
+    const int nkt = K / 64;
+    const int kt = (int)(tk % nkt);
+    const long long et = tk / nkt;               // (e, tn)
+    const int ntn = N / BN;
+    const int tn = (int)(et % ntn);
+    const int e = (int)(et / ntn);
+    const int row = I > 0 ? (j < BN / 2 ? tn * (BN / 2) + j : I + tn * (BN / 2) + (j - BN / 2))
+                          : tn * BN + j;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(w + ((long long)e * N + row) * K + kt * 64 + b);
+    *reinterpret_cast<u32x4*>(out + byte) = v;
+  }
+}
+
 // Tile shapes (N a multiple of 256 takes the LDS-DMA kernels):
 //   bf16: 256x256 tiles, 8 waves of 128x64 in ping-pong, BK=64;
 //   fp8 weights, gate/up: 96x512 tiles (a decode batch's ~50-90 rows per
@@ -1713,6 +1759,7 @@ GemmParams common_params(const FfnArgs& a) {
   g.E = a.E;
   g.layers = a.layers;
   g.e_layer = a.e_layer;
+  g.tiled = a.tiled;
   return g;
 }
 
@@ -1722,6 +1769,17 @@ bool small_rows(const FfnArgs& a) {
 }
 
 }  // namespace
+
+hipError_t launch_tile_weights_fp8(const uint8_t* w, uint8_t* out, int E, int N, int K, int I,
+                                   hipStream_t stream) {
+  const int BN = fp8_tile_width(I > 0, N);
+  if (E <= 0 || N % BN || K % 128) return hipErrorInvalidValue;
+  const long long chunks = (long long)E * N * K / 16;
+  const long long blocks = std::min<long long>((chunks + 255) / 256, 65536);
+  hipLaunchKernelGGL(tile_weights_fp8_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, w, out,
+                     E, N, K, I, BN);
+  return hipGetLastError();
+}
 
 hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream) {
   // [R,H] x [2I,H]^T -> h [R,I]

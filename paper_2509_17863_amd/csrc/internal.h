@@ -54,6 +54,8 @@ struct FfnArgs {
   const float* xs = nullptr;    // [T,H/128]
   uint8_t* hq = nullptr;        // [R,I]
   float* hs = nullptr;          // [R,I/128]
+  // fp8 weights stored in the tiled layout of launch_tile_weights_fp8
+  bool tiled = false;
 };
 
 // x [rows,K] bf16 -> q [rows,K] e4m3fn and s [rows,K/128]: per row and 128
@@ -61,6 +63,12 @@ struct FfnArgs {
 // saturating).
 hipError_t launch_quantize_rows(const uint16_t* x, long long rows, int K, uint8_t* q, float* s,
                                 hipStream_t stream);
+
+// fp8 weights [E,N,K] -> the tiled layout the fp8-weight ring kernels read
+// (weight stages contiguous).  I > 0: a gate/up matrix (N = 2I, gate rows then
+// up rows); I == 0: a down matrix.
+hipError_t launch_tile_weights_fp8(const uint8_t* w, uint8_t* out, int E, int N, int K, int I,
+                                   hipStream_t stream);
 
 // Gate/up GEMM with the SiLU*mul epilogue into h.
 hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream);

@@ -24,11 +24,12 @@ __all__ = [
     "EAAS_WS_H", "EAAS_WS_HQ", "EAAS_WS_HS", "EAAS_WS_XQ", "EAAS_WS_XS", "EAAS_WS_STAGE",
     "eaas_workspace_bytes_for", "EAAS_ENTRY_ROUTE_PERMUTE", "EAAS_ENTRY_FFN_GROUPED",
     "EAAS_ENTRY_FORWARD", "eaas_expert_forward_noalloc", "EAAS_NOALLOC_SCRATCH_BYTES",
-    "use_library",
+    "use_library", "EAAS_FP8_E4M3_TILED", "EAAS_GATE_UP", "EAAS_DOWN", "eaas_tile_weights_fp8",
 ]
 
 EAAS_OK = 0
-EAAS_BF16, EAAS_FP8_E4M3, EAAS_FP32, EAAS_FP8_E4M3_A8 = 0, 1, 2, 3
+EAAS_BF16, EAAS_FP8_E4M3, EAAS_FP32, EAAS_FP8_E4M3_A8, EAAS_FP8_E4M3_TILED = 0, 1, 2, 3, 4
+EAAS_GATE_UP, EAAS_DOWN = 0, 1
 EAAS_SLOT_EMPTY, EAAS_SLOT_READY, EAAS_SLOT_DONE, EAAS_SLOT_OFFLINE = 0, 1, 2, 3
 EAAS_WS_H, EAAS_WS_HQ, EAAS_WS_HS, EAAS_WS_XQ, EAAS_WS_XS, EAAS_WS_STAGE = range(6)
 EAAS_ENTRY_ROUTE_PERMUTE, EAAS_ENTRY_FFN_GROUPED, EAAS_ENTRY_FORWARD = range(3)
@@ -38,7 +39,7 @@ EXPORTED = ("eaas_workspace_bytes", "eaas_route_permute", "eaas_expert_ffn_group
             "eaas_status_string", "eaas_segments_workspace_bytes",
             "eaas_expert_forward_segments", "eaas_server_workspace_bytes", "eaas_server_step",
             "eaas_quantize_rows_fp8", "eaas_workspace_region", "eaas_workspace_bytes_for",
-            "eaas_expert_forward_noalloc")
+            "eaas_expert_forward_noalloc", "eaas_tile_weights_fp8")
 
 _DEFAULT_LIB = Path(__file__).resolve().parent / "libeaas.so"
 _LIB_PATH = _DEFAULT_LIB
@@ -96,6 +97,8 @@ def _bind(L: ctypes.CDLL) -> ctypes.CDLL:
     L.eaas_server_workspace_bytes.restype = sz
     L.eaas_server_step.argtypes = [sp, vp, i32, vp, i32, i32, vp, sz, vp]
     L.eaas_server_step.restype = i32
+    L.eaas_tile_weights_fp8.argtypes = [sp, i32, vp, vp, vp]
+    L.eaas_tile_weights_fp8.restype = i32
     L.eaas_quantize_rows_fp8.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, vp, vp, vp]
     L.eaas_quantize_rows_fp8.restype = i32
     L.eaas_workspace_region.argtypes = [sp, i32, i32, ctypes.POINTER(sz), ctypes.POINTER(sz)]
@@ -162,11 +165,13 @@ def _check(status: int, where: str) -> None:
         raise EaasError(status, where)
 
 
-def _wdtype(w: torch.Tensor, act8: bool = False) -> int:
+def _wdtype(w: torch.Tensor, act8: bool = False, tiled: bool = False) -> int:
     if w.element_size() == 1:
-        return EAAS_FP8_E4M3_A8 if act8 else EAAS_FP8_E4M3
-    if act8:
-        raise ValueError("fp8 activations need fp8-e4m3 (1-byte) weights")
+        if act8 and tiled:
+            raise ValueError("the tiled weight layout is for fp8 weights with bf16 activations")
+        return EAAS_FP8_E4M3_A8 if act8 else (EAAS_FP8_E4M3_TILED if tiled else EAAS_FP8_E4M3)
+    if act8 or tiled:
+        raise ValueError("fp8 activations and the tiled layout need fp8-e4m3 (1-byte) weights")
     if w.element_size() == 2:
         return EAAS_BF16
     raise ValueError("weights must be bf16 (2-byte) or fp8-e4m3 (1-byte) tensors")
@@ -192,6 +197,19 @@ def eaas_quantize_rows_fp8(x: torch.Tensor, q: torch.Tensor, s: torch.Tensor, st
     rows, K = x.shape
     _check(lib().eaas_quantize_rows_fp8(_p(x), rows, K, _p(q), _p(s), _stream(stream)),
            "eaas_quantize_rows_fp8")
+
+
+def eaas_tile_weights_fp8(w: torch.Tensor, which: int, H: int, I: int, out: torch.Tensor,
+                          stream=None) -> None:
+    """fp8 weights [E,N,K] (which = EAAS_GATE_UP: N = 2I, K = H; EAAS_DOWN:
+    N = H, K = I) -> `out`, the same bytes in the tiled layout of
+    EAAS_FP8_E4M3_TILED."""
+    E = w.shape[0]
+    s = _shape(0, H, I, E, 1)
+    if out.numel() * out.element_size() != w.numel() * w.element_size():
+        raise ValueError("out must hold as many bytes as w")
+    _check(lib().eaas_tile_weights_fp8(ctypes.byref(s), int(which), _p(w), _p(out), _stream(stream)),
+           "eaas_tile_weights_fp8")
 
 
 def eaas_workspace_bytes(T, H, I, E, k, w_dtype=EAAS_BF16) -> int:
@@ -230,15 +248,15 @@ def eaas_route_permute(topk_ids: torch.Tensor, E: int, routing: dict, ws: torch.
 def eaas_expert_ffn_grouped(x: torch.Tensor, routing: dict, w_gate_up: torch.Tensor,
                             w_down: torch.Tensor, y_perm: torch.Tensor, ws: torch.Tensor,
                             k: int, w_gate_up_scale=None, w_down_scale=None, stream=None,
-                            act8: bool = False) -> None:
+                            act8: bool = False, tiled: bool = False) -> None:
     T, H = x.shape
     E, twoI, _ = w_gate_up.shape
     s = _shape(T, H, twoI // 2, E, k)
     r = _routing(routing)
     st = lib().eaas_expert_ffn_grouped(
         ctypes.byref(s), _p(x), ctypes.byref(r), _p(w_gate_up), _p(w_gate_up_scale),
-        _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8), _p(y_perm), _p(ws), ws.numel(),
-        _stream(stream))
+        _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8, tiled), _p(y_perm), _p(ws),
+        ws.numel(), _stream(stream))
     _check(st, "eaas_expert_ffn_grouped")
 
 
@@ -258,10 +276,11 @@ def eaas_expert_forward(x: torch.Tensor, topk_ids: torch.Tensor, topk_weights: t
                         w_gate_up: torch.Tensor, w_down: torch.Tensor, out: torch.Tensor,
                         ws: torch.Tensor, w_gate_up_scale=None, w_down_scale=None,
                         routing: dict | None = None, stream=None, events=None,
-                        act8: bool = False) -> None:
+                        act8: bool = False, tiled: bool = False) -> None:
     """events: optional 5 torch.cuda.Event(enable_timing=True) recorded on the
     stream around routing, gate/up, down and combine (profiled entry point).
-    act8: fp8 activations with the fp8 weights (EAAS_FP8_E4M3_A8)."""
+    act8: fp8 activations with the fp8 weights (EAAS_FP8_E4M3_A8).
+    tiled: the fp8 weights are in the layout of eaas_tile_weights_fp8."""
     T, H = x.shape
     E, twoI, _ = w_gate_up.shape
     k = topk_ids.shape[1]
@@ -269,8 +288,9 @@ def eaas_expert_forward(x: torch.Tensor, topk_ids: torch.Tensor, topk_weights: t
     r = _routing(routing)
     odt = EAAS_FP32 if out.dtype == torch.float32 else EAAS_BF16
     args = (ctypes.byref(s), _p(x), _p(topk_ids), _p(topk_weights), _p(w_gate_up),
-            _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8), _p(out), odt,
-            ctypes.byref(r) if r is not None else None, _p(ws), ws.numel(), _stream(stream))
+            _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8, tiled),
+            _p(out), odt, ctypes.byref(r) if r is not None else None, _p(ws), ws.numel(),
+            _stream(stream))
     if events is None:
         _check(lib().eaas_expert_forward(*args), "eaas_expert_forward")
         return
@@ -284,7 +304,7 @@ def eaas_expert_forward_noalloc(x: torch.Tensor, topk_ids: torch.Tensor,
                                 topk_weights: torch.Tensor, w_gate_up: torch.Tensor,
                                 w_down: torch.Tensor, out: torch.Tensor, w_gate_up_scale=None,
                                 w_down_scale=None, routing: dict | None = None, stream=None,
-                                act8: bool = False) -> None:
+                                act8: bool = False, tiled: bool = False) -> None:
     """eaas_expert_forward on the library's own per-GPU scratch array: no
     workspace argument, nothing allocated (shapes up to
     EAAS_NOALLOC_SCRATCH_BYTES of workspace)."""
@@ -296,8 +316,8 @@ def eaas_expert_forward_noalloc(x: torch.Tensor, topk_ids: torch.Tensor,
     odt = EAAS_FP32 if out.dtype == torch.float32 else EAAS_BF16
     _check(lib().eaas_expert_forward_noalloc(
         ctypes.byref(s), _p(x), _p(topk_ids), _p(topk_weights), _p(w_gate_up),
-        _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8), _p(out), odt,
-        ctypes.byref(r) if r is not None else None, _stream(stream)),
+        _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8, tiled), _p(out),
+        odt, ctypes.byref(r) if r is not None else None, _stream(stream)),
         "eaas_expert_forward_noalloc")
 
 
@@ -336,7 +356,7 @@ def eaas_expert_forward_segments(table: torch.Tensor, num_tokens: torch.Tensor, 
                                  capacity: int, k: int, w_gate_up: torch.Tensor,
                                  w_down: torch.Tensor, ws: torch.Tensor, out_dtype=EAAS_BF16,
                                  w_gate_up_scale=None, w_down_scale=None, stream=None,
-                                 act8: bool = False) -> None:
+                                 act8: bool = False, tiled: bool = False) -> None:
     """The step on a dynamic batch: `table` from segment_table, `num_tokens`
     a device int32 tensor of the requests' token counts (read on the device),
     `capacity` the bound on their sum.  act8: fp8 activations."""
@@ -344,7 +364,7 @@ def eaas_expert_forward_segments(table: torch.Tensor, num_tokens: torch.Tensor, 
     s = _shape(capacity, H, twoI // 2, E, k)
     st = lib().eaas_expert_forward_segments(
         ctypes.byref(s), _p(table), _p(num_tokens), int(n_seg), _p(w_gate_up),
-        _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8),
+        _p(w_gate_up_scale), _p(w_down), _p(w_down_scale), _wdtype(w_gate_up, act8, tiled),
         int(out_dtype), _p(ws), ws.numel(), _stream(stream))
     _check(st, "eaas_expert_forward_segments")
 

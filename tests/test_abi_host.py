@@ -272,3 +272,26 @@ def test_k_above_E_is_a_valid_shape():
     r = _routing()
     # validation passes the shape and stops at the missing workspace
     assert L.eaas_route_permute(ctypes.byref(s), FAKE, ctypes.byref(r), None, 0, None) == -3
+
+
+def test_tiled_fp8_dtype_and_tile_entry_validation():
+    """EAAS_FP8_E4M3_TILED: the fp8 workspace, H a multiple of 256; the
+    tiling entry point rejects bad arguments on the host."""
+    T8 = eaas.EAAS_FP8_E4M3_TILED
+    assert eaas.eaas_workspace_bytes(64, 512, 256, 8, 2, T8) == \
+        eaas.eaas_workspace_bytes(64, 512, 256, 8, 2, eaas.EAAS_FP8_E4M3)
+    assert eaas.eaas_workspace_bytes(64, 384, 256, 8, 2, T8) == 0
+    L = eaas.lib()
+    s = shape(H=512, I=256)
+    assert L.eaas_tile_weights_fp8(None, 0, FAKE, FAKE * 64, None) == -1
+    assert L.eaas_tile_weights_fp8(ctypes.byref(s), 2, FAKE, FAKE * 64, None) == -1
+    assert L.eaas_tile_weights_fp8(ctypes.byref(s), 0, None, FAKE * 64, None) == -1
+    assert L.eaas_tile_weights_fp8(ctypes.byref(s), 0, FAKE + 8, FAKE * 64, None) == -1
+    assert L.eaas_tile_weights_fp8(ctypes.byref(s), 0, FAKE, FAKE + 4096, None) == -1  # overlap
+    assert L.eaas_tile_weights_fp8(ctypes.byref(s), 1, FAKE, FAKE, None) == -1         # in place
+    bad = shape(H=384, I=256)
+    assert L.eaas_tile_weights_fp8(ctypes.byref(bad), 0, FAKE, FAKE * 64, None) == -2
+    # the fp8 scales are required as for row-major fp8 weights
+    big = 1 << 34
+    assert L.eaas_expert_forward(ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, None, FAKE, None, T8,
+                                 FAKE * 64, 0, None, FAKE, big, None) == -1
