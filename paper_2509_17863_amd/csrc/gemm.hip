@@ -139,6 +139,9 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "me
 // are wave-uniform (SGPRs; `lds` goes to M0).
 // The base is passed through readfirstlane so it is held in SGPRs even where
 // the compiler cannot prove it uniform (free when it already is).
+// NT sets the nontemporal cache policy: used for weight stages that few other
+// tiles of the launch read (see stream_weights_once), so they do not displace
+// the reused token rows in L2 and the MALL.
 __device__ __forceinline__ const void* wave_uniform(const void* p) {
   const uint64_t v = reinterpret_cast<uintptr_t>(p);
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
@@ -146,9 +149,14 @@ __device__ __forceinline__ const void* wave_uniform(const void* p) {
   return reinterpret_cast<const void*>(((uint64_t)hi << 32) | lo);
 }
 
+template <bool NT = false>
 __device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-               :: "v"(voff), "s"(wave_uniform(base)), "s"(lds) : "memory");
+  if constexpr (NT)
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 nt"
+                 :: "v"(voff), "s"(wave_uniform(base)), "s"(lds) : "memory");
+  else
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :: "v"(voff), "s"(wave_uniform(base)), "s"(lds) : "memory");
 }
 
 // Scheduler variant, fixed at build time (the default library is built with
@@ -500,7 +508,7 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16(u32x2 q) {
 }
 
 template <int KIND, int BK, int SA, int SB, int BSPAN, int NW, int BM, int BN, int MBW, int NBW,
-          bool FULL, bool FP8>
+          bool FULL, bool FP8, bool NTB>
 struct DmaLoop {
   static constexpr int RB = BK * 2;            // bytes per LDS row of A (bf16)
   static constexpr int CH = RB / 16;           // 16-byte chunks per A row
@@ -556,7 +564,7 @@ struct DmaLoop {
               s.lds + (ka % SA) * A_BYTES + a_inst(s.wave, q) * RPI * RB);
     } else {
       if (kb >= 0 && kb < nb)
-        dma16(s.b + (size_t)kb * s.b_kstride, s.b_off[q - A_INST],
+        dma16<NTB>(s.b + (size_t)kb * s.b_kstride, s.b_off[q - A_INST],
               s.lds + B_BASE + (kb % SB) * B_BYTES + b_inst(s.wave, q - A_INST) * BRPI * BRB);
     }
   }
@@ -762,7 +770,7 @@ struct DmaLoop {
 // OCC: workgroups per CU the launch is sized for (the LDS footprint must
 // allow it); it sets the waves per SIMD the registers are budgeted for.
 template <int KIND, bool FP8, int BK, int SA, int SB, int BSPAN, int WM, int WN, int MBW, int NBW,
-          int OCC>
+          int OCC, bool NTB>
 __global__ __launch_bounds__(WM * WN * kWave)
 __attribute__((amdgpu_waves_per_eu(WM * WN * OCC / 4, WM * WN * OCC / 4)))
 void grouped_gemm_dma_kernel(GemmParams p) {
@@ -771,8 +779,8 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   constexpr int BM = WM * MBW * 32, BN = WN * NBW * 32;
   constexpr bool GATEUP = KIND == kGateUp;
   static_assert(!GATEUP || (NBW % 2 == 0), "gate/up pairs gate and up blocks");
-  using Full = DmaLoop<KIND, BK, SA, SB, BSPAN, NW, BM, BN, MBW, NBW, true, FP8>;
-  using Part = DmaLoop<KIND, BK, SA, SB, BSPAN, NW, BM, BN, MBW, NBW, false, FP8>;
+  using Full = DmaLoop<KIND, BK, SA, SB, BSPAN, NW, BM, BN, MBW, NBW, true, FP8, NTB>;
+  using Part = DmaLoop<KIND, BK, SA, SB, BSPAN, NW, BM, BN, MBW, NBW, false, FP8, NTB>;
   constexpr int RB = Full::RB, CH = Full::CH, RPI = Full::RPI;
   constexpr int BRB = Full::BRB, BCH = Full::BCH, BRPI = Full::BRPI;
 
@@ -1057,6 +1065,16 @@ inline long long grid_tiles(int R, int E, int BM, int BN, int N) {
   return mt * (N / BN);
 }
 
+// Whether the weight stages are read with the nontemporal policy: when the
+// R slots fill at most about two BM-row tiles per resident expert, each weight
+// tile is read by at most a couple of tiles of the launch, and keeping it out
+// of the caches' reuse leaves them to the token rows (measured: faster on the
+// qwen3 shape and decode-sized batches, slower on mixtral's and the DeepSeek
+// prefill shard's, whose experts hold 4 and 16 tiles).  Results do not change.
+inline bool stream_weights_once(int R, int E, int BM) {
+  return (long long)R <= 2LL * BM * E;
+}
+
 template <int KIND, bool FP8, int WM, int WN, int MBW, int NBW>
 hipError_t launch_reg(const GemmParams& p, int R, int E, hipStream_t stream) {
   constexpr int BM = WM * MBW * 32;
@@ -1073,13 +1091,19 @@ template <int KIND, bool FP8, int BK, int SA, int SB, int BSPAN, int WM, int WN,
           int OCC = 1>
 hipError_t launch_dma(const GemmParams& p, int R, int E, hipStream_t stream) {
   constexpr int BM = WM * MBW * 32, BN = WN * NBW * 32;
-  using Loop = DmaLoop<KIND, BK, SA, SB, BSPAN, WM * WN, BM, BN, MBW, NBW, true, FP8>;
+  using Loop = DmaLoop<KIND, BK, SA, SB, BSPAN, WM * WN, BM, BN, MBW, NBW, true, FP8, false>;
   static_assert(OCC * Loop::LDS_BYTES <= 160 * 1024 - OCC * 1024, "workgroups per CU must fit in LDS");
   const long long grid = grid_tiles(R, E, BM, BN, p.N);
   if (grid <= 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((grouped_gemm_dma_kernel<KIND, FP8, BK, SA, SB, BSPAN, WM, WN, MBW, NBW, OCC>),
-                     dim3((unsigned)grid), dim3(WM * WN * kWave), 0, stream, p);
+  if (stream_weights_once(R, E, BM))
+    hipLaunchKernelGGL(
+        (grouped_gemm_dma_kernel<KIND, FP8, BK, SA, SB, BSPAN, WM, WN, MBW, NBW, OCC, true>),
+        dim3((unsigned)grid), dim3(WM * WN * kWave), 0, stream, p);
+  else
+    hipLaunchKernelGGL(
+        (grouped_gemm_dma_kernel<KIND, FP8, BK, SA, SB, BSPAN, WM, WN, MBW, NBW, OCC, false>),
+        dim3((unsigned)grid), dim3(WM * WN * kWave), 0, stream, p);
   return hipGetLastError();
 }
 
@@ -1108,7 +1132,7 @@ hipError_t launch_dma(const GemmParams& p, int R, int E, hipStream_t stream) {
 // its DMA was issued, B three).  The MFMA order per accumulator is the same
 // as in the other GEMM loops: k-steps ascending within a tile, tiles
 // ascending, so results do not depend on which loop ran.
-template <int KIND>
+template <int KIND, bool NTB>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void grouped_gemm_pp_kernel(GemmParams p) {
   constexpr int BM = 256, BN = 256, BK = 64, MBW = 4, NBW = 2, NT = 512;
@@ -1172,7 +1196,10 @@ void grouped_gemm_pp_kernel(GemmParams p) {
     const uint32_t dst = grp == 0 ? lds0 + (kt % SA) * A_BYTES + w4 * 8 * RB
                                   : lds0 + B_BASE + (kt % SB) * B_BYTES + w4 * 8 * RB;
 #pragma unroll
-    for (int q = 0; q < INST; ++q) dma16(src, doff[q], dst + q * 4 * 8 * RB);
+    for (int q = 0; q < INST; ++q) {
+      if (grp == 0) dma16(src, doff[q], dst + q * 4 * 8 * RB);
+      else dma16<NTB>(src, doff[q], dst + q * 4 * 8 * RB);
+    }
   };
 
   const int wn = w4;
@@ -1297,8 +1324,12 @@ hipError_t launch_pp(const GemmParams& p, int R, int E, hipStream_t stream) {
   const long long grid = grid_tiles(R, E, 256, 256, p.N);
   if (grid <= 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((grouped_gemm_pp_kernel<KIND>), dim3((unsigned)grid), dim3(512), 0, stream,
-                     p);
+  if (stream_weights_once(R, E, 256))
+    hipLaunchKernelGGL((grouped_gemm_pp_kernel<KIND, true>), dim3((unsigned)grid), dim3(512), 0,
+                       stream, p);
+  else
+    hipLaunchKernelGGL((grouped_gemm_pp_kernel<KIND, false>), dim3((unsigned)grid), dim3(512), 0,
+                       stream, p);
   return hipGetLastError();
 }
 
@@ -1363,7 +1394,7 @@ struct W8Tile {
   static constexpr int AS_CHUNKS = BM / 64;  // 64-row chunks of row scales
 };
 
-template <int KIND, int MB>
+template <int KIND, int MB, bool NTB>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void grouped_gemm_w8a8_kernel(GemmParams p) {
   using T8 = W8Tile<MB>;
@@ -1436,7 +1467,7 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
     } else {
       const uint32_t dst = lds0 + B_BASE + (kt % SB) * B_BYTES + wn * 8 * RB;
 #pragma unroll
-      for (int q = 0; q < B_INST; ++q) dma16(dbase + kt * RB, doff[q], dst + q * 4 * 8 * RB);
+      for (int q = 0; q < B_INST; ++q) dma16<NTB>(dbase + kt * RB, doff[q], dst + q * 4 * 8 * RB);
     }
   };
 
@@ -1662,8 +1693,12 @@ hipError_t launch_w8a8_mb(const GemmParams& p, int R, int E, hipStream_t stream)
   const long long grid = grid_tiles(R, E, T8::BM, T8::BN, p.N);
   if (grid <= 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((grouped_gemm_w8a8_kernel<KIND, MB>), dim3((unsigned)grid), dim3(T8::NT), 0,
-                     stream, p);
+  if (stream_weights_once(R, E, T8::BM))
+    hipLaunchKernelGGL((grouped_gemm_w8a8_kernel<KIND, MB, true>), dim3((unsigned)grid),
+                       dim3(T8::NT), 0, stream, p);
+  else
+    hipLaunchKernelGGL((grouped_gemm_w8a8_kernel<KIND, MB, false>), dim3((unsigned)grid),
+                       dim3(T8::NT), 0, stream, p);
   return hipGetLastError();
 }
 
