@@ -590,10 +590,15 @@ def main() -> int:
     if not args.no_decode and args.decode_workload != args.workload:
         del dev
         torch.cuda.empty_cache()
-        rd, _, _, _ = measure(args.decode_workload, max(args.steps, 200), args.warmup,
+        # a decode step is 0.3-0.4 ms: 200 warm-up and 200 timed steps, so the
+        # figure is taken with the engine clock settled (it starts from idle
+        # and a few milliseconds of short steps do not bring it up)
+        rd, _, _, _ = measure(args.decode_workload, max(args.steps, 200), max(args.warmup, 200),
                               tiled_fp8=not args.row_major_fp8)
         rd.pop("_tiled", None)
         res["decode"] = decode_summary(rd)
+        res["decode"]["steps"] = max(args.steps, 200)
+        res["decode"]["warmup"] = max(args.warmup, 200)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(d)
     print(json.dumps(res), flush=True)
