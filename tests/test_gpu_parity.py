@@ -85,6 +85,8 @@ ROUTE_CASES = [
     # around the single-workgroup path's limit of 8192 slots
     (1024, 16, 4, 0.2, 9), (8192, 1024, 1, 0.1, 10), (8193, 7, 1, 0.0, 11), (1, 1024, 8, 0.5, 12),
     (4096, 8, 2, 0.0, 13),
+    # the largest k (64): many slots per token
+    (50, 32, 64, 0.1, 14), (129, 1024, 64, 0.0, 15),
 ]
 
 
@@ -127,6 +129,8 @@ SMALL = [
     (130, 512, 256, 4, 3, 25, None, "fp8", 0.0),     # fp8 block-scaled weights
     (600, 768, 512, 3, 2, 26, None, "fp8", 0.2),     # fp8, several tiles, masked
     (200, 384, 384, 5, 2, 27, 1.5, "fp8", 0.1),      # fp8, gate/up N = 768, down N = 384
+    (40, 256, 128, 80, 64, 28, None, "bf16", 0.05),  # the largest k: 64 slots per token
+    (24, 512, 256, 72, 64, 29, 1.2, "fp8", 0.0),     # the largest k, fp8 weights
 ]
 
 
