@@ -508,7 +508,7 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16(u32x2 q) {
 }
 
 template <int KIND, int BK, int SA, int SB, int BSPAN, int NW, int BM, int BN, int MBW, int NBW,
-          bool FULL, bool FP8, bool NTB>
+          bool FULL, bool FP8>
 struct DmaLoop {
   static constexpr int RB = BK * 2;            // bytes per LDS row of A (bf16)
   static constexpr int CH = RB / 16;           // 16-byte chunks per A row
@@ -564,7 +564,7 @@ struct DmaLoop {
               s.lds + (ka % SA) * A_BYTES + a_inst(s.wave, q) * RPI * RB);
     } else {
       if (kb >= 0 && kb < nb)
-        dma16<NTB>(s.b + (size_t)kb * s.b_kstride, s.b_off[q - A_INST],
+        dma16(s.b + (size_t)kb * s.b_kstride, s.b_off[q - A_INST],
               s.lds + B_BASE + (kb % SB) * B_BYTES + b_inst(s.wave, q - A_INST) * BRPI * BRB);
     }
   }
@@ -770,7 +770,7 @@ struct DmaLoop {
 // OCC: workgroups per CU the launch is sized for (the LDS footprint must
 // allow it); it sets the waves per SIMD the registers are budgeted for.
 template <int KIND, bool FP8, int BK, int SA, int SB, int BSPAN, int WM, int WN, int MBW, int NBW,
-          int OCC, bool NTB>
+          int OCC>
 __global__ __launch_bounds__(WM * WN * kWave)
 __attribute__((amdgpu_waves_per_eu(WM * WN * OCC / 4, WM * WN * OCC / 4)))
 void grouped_gemm_dma_kernel(GemmParams p) {
@@ -779,8 +779,8 @@ void grouped_gemm_dma_kernel(GemmParams p) {
   constexpr int BM = WM * MBW * 32, BN = WN * NBW * 32;
   constexpr bool GATEUP = KIND == kGateUp;
   static_assert(!GATEUP || (NBW % 2 == 0), "gate/up pairs gate and up blocks");
-  using Full = DmaLoop<KIND, BK, SA, SB, BSPAN, NW, BM, BN, MBW, NBW, true, FP8, NTB>;
-  using Part = DmaLoop<KIND, BK, SA, SB, BSPAN, NW, BM, BN, MBW, NBW, false, FP8, NTB>;
+  using Full = DmaLoop<KIND, BK, SA, SB, BSPAN, NW, BM, BN, MBW, NBW, true, FP8>;
+  using Part = DmaLoop<KIND, BK, SA, SB, BSPAN, NW, BM, BN, MBW, NBW, false, FP8>;
   constexpr int RB = Full::RB, CH = Full::CH, RPI = Full::RPI;
   constexpr int BRB = Full::BRB, BCH = Full::BCH, BRPI = Full::BRPI;
 
@@ -1065,13 +1065,13 @@ inline long long grid_tiles(int R, int E, int BM, int BN, int N) {
   return mt * (N / BN);
 }
 
-// Whether the weight stages are read with the nontemporal policy: when the
-// R slots fill at most one BM-row tile per resident expert on average (a
-// decode-sized batch), each weight tile is read once in the launch, and
-// keeping it out of the caches' reuse leaves them to the token rows
-// (measured: bf16 weights 4% and fp8 x fp8 6% faster on such batches; on
-// the 512-slots-per-expert qwen3 shape, two tiles per expert, 1% slower).
-// Results do not change.
+// Whether the bf16 ping-pong and the fp8 x fp8 loop read their weight
+// stages with the nontemporal policy: when the R slots fill at most one
+// BM-row tile per resident expert on average (a decode-sized batch), each
+// weight tile is read once in the launch, and keeping it out of the caches'
+// reuse leaves them to the token rows (measured: steps 5% and 8% faster on
+// such batches; on the 512-slots-per-expert qwen3 shape, two tiles per
+// expert, 1% slower).  Results do not change.
 inline bool stream_weights_once(int R, int E, int BM) {
   return (long long)R <= (long long)BM * E;
 }
@@ -1092,19 +1092,18 @@ template <int KIND, bool FP8, int BK, int SA, int SB, int BSPAN, int WM, int WN,
           int OCC = 1>
 hipError_t launch_dma(const GemmParams& p, int R, int E, hipStream_t stream) {
   constexpr int BM = WM * MBW * 32, BN = WN * NBW * 32;
-  using Loop = DmaLoop<KIND, BK, SA, SB, BSPAN, WM * WN, BM, BN, MBW, NBW, true, FP8, false>;
+  using Loop = DmaLoop<KIND, BK, SA, SB, BSPAN, WM * WN, BM, BN, MBW, NBW, true, FP8>;
   static_assert(OCC * Loop::LDS_BYTES <= 160 * 1024 - OCC * 1024, "workgroups per CU must fit in LDS");
   const long long grid = grid_tiles(R, E, BM, BN, p.N);
   if (grid <= 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
-  if (stream_weights_once(R, E, BM))
-    hipLaunchKernelGGL(
-        (grouped_gemm_dma_kernel<KIND, FP8, BK, SA, SB, BSPAN, WM, WN, MBW, NBW, OCC, true>),
-        dim3((unsigned)grid), dim3(WM * WN * kWave), 0, stream, p);
-  else
-    hipLaunchKernelGGL(
-        (grouped_gemm_dma_kernel<KIND, FP8, BK, SA, SB, BSPAN, WM, WN, MBW, NBW, OCC, false>),
-        dim3((unsigned)grid), dim3(WM * WN * kWave), 0, stream, p);
+  // (the fp8 ring reads weights with the default policy: row-major fp8 rows
+  // are read 64 bytes of each 128-byte line per K tile, the other half one K
+  // tile later, and a nontemporal line may be gone by then (measured:
+  // dsv3_decode gate/up 0.21 -> 0.26 ms); on the tiled layout the hint
+  // changed nothing, and with Zipf routing it slowed the down projection 7%)
+  hipLaunchKernelGGL((grouped_gemm_dma_kernel<KIND, FP8, BK, SA, SB, BSPAN, WM, WN, MBW, NBW, OCC>),
+                     dim3((unsigned)grid), dim3(WM * WN * kWave), 0, stream, p);
   return hipGetLastError();
 }
 
