@@ -369,6 +369,21 @@ def test_token_permutation_equivariance_bitwise(gpu):
     assert np.array_equal(a[p].view(np.uint32), b.view(np.uint32))
 
 
+@pytest.mark.parametrize("wdtype", ["bf16", "fp8"])
+def test_batch_split_invariance_bitwise(gpu, wdtype):
+    """A token's output does not depend on the batch around it: the first
+    64 tokens alone (a decode-sized batch: at most one M tile per expert,
+    nontemporal weight reads for bf16) give the same bits as inside the
+    whole 4096-token batch (several M tiles per expert, default reads), and
+    so does a 300-token slice from the middle."""
+    d = synth.make_inputs(4096, 512, 256, 8, 2, 34, zipf=1.1, wdtype=wdtype)
+    say("batch split", wdtype)
+    whole = forward(to_device(d), d["k"]).cpu().numpy()
+    for lo, hi in ((0, 64), (1800, 2100)):
+        part = forward(to_device(O.sub_batch(d, np.arange(lo, hi))), d["k"]).cpu().numpy()
+        assert np.array_equal(part.view(np.uint32), whole[lo:hi].view(np.uint32)), (lo, hi)
+
+
 def test_graph_replay_matches_eager(gpu):
     d = _mid_inputs(seed=34)
     dev = to_device(d)
