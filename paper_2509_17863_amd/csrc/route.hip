@@ -80,10 +80,18 @@ __global__ __launch_bounds__(kScanThreads) void route_scan_kernel(
   const int e = threadIdx.x;  // E <= 1024 = blockDim
   int c = 0;
   if (e < E) {
-    for (int b = 0; b < nblk; ++b) {
-      const int v = hist[(size_t)b * E + e];
-      hist[(size_t)b * E + e] = c;  // rows of e in chunks before b
-      c += v;
+    // the loads of a batch of chunks are issued together, ahead of the
+    // stores: one memory round trip per kBatch chunks instead of per chunk
+    constexpr int kBatch = 16;
+    for (int b0 = 0; b0 < nblk; b0 += kBatch) {
+      int v[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) v[u] = b0 + u < nblk ? hist[(size_t)(b0 + u) * E + e] : 0;
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        if (b0 + u < nblk) hist[(size_t)(b0 + u) * E + e] = c;  // rows of e in chunks before b
+        c += v[u];
+      }
     }
   }
   int valid_total;
