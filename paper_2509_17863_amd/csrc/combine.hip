@@ -19,8 +19,20 @@ namespace {
 constexpr int kCombineThreads = 256;
 constexpr int kCombineCols = kCombineThreads * 4;  // columns per workgroup
 
+// One slot's staged row: the weighted product already (BY_SLOT, at row s) or
+// the unweighted expert output (at row inv[s]).
+template <bool BY_SLOT>
+__device__ __forceinline__ f32x4 load_slot(const float* __restrict__ y, int s, int row, int H,
+                                           int c) {
+  if (BY_SLOT)
+    return __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(y + (size_t)s * H + c));
+  return *reinterpret_cast<const f32x4*>(y + (size_t)row * H + c);
+}
+
 // grid: (T, ceil(H / kCombineCols)); each thread owns 4 consecutive columns.
-template <bool BY_SLOT, bool OUT_FP32>
+// KU > 0 (k <= KU): the k rows are all requested before the first add, so a
+// thread has k loads in flight; the adds still run in ascending j.
+template <bool BY_SLOT, bool OUT_FP32, int KU>
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(
     const float* __restrict__ y, const int32_t* __restrict__ inv,
     const float* __restrict__ w, int T, int H, int k, void* __restrict__ out) {
@@ -30,20 +42,36 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(
   const int c = blockIdx.y * kCombineCols + threadIdx.x * 4;
   if (c >= H) return;
   f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int j = 0; j < k; ++j) {
-    const int s = t * k + j;
-    const int row = inv[s];
-    if (row < 0 || row >= T * k) continue;
+  auto add = [&](const f32x4& v, int s) {
+#pragma clang fp contract(off)
     if (BY_SLOT) {
-      const f32x4 v = __builtin_nontemporal_load(
-          reinterpret_cast<const f32x4*>(y + (size_t)s * H + c));
 #pragma unroll
       for (int q = 0; q < 4; ++q) acc[q] = acc[q] + v[q];
     } else {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(y + (size_t)row * H + c);
       const float wj = w[s];
 #pragma unroll
       for (int q = 0; q < 4; ++q) acc[q] = acc[q] + wj * v[q];
+    }
+  };
+  if constexpr (KU > 0) {
+    f32x4 v[KU];
+    bool live[KU];
+#pragma unroll
+    for (int j = 0; j < KU; ++j) {
+      const int s = t * k + j;
+      const int row = j < k ? inv[s] : -1;
+      live[j] = row >= 0 && row < T * k;
+      v[j] = live[j] ? load_slot<BY_SLOT>(y, s, row, H, c) : f32x4{};
+    }
+#pragma unroll
+    for (int j = 0; j < KU; ++j)
+      if (live[j]) add(v[j], t * k + j);
+  } else {
+    for (int j = 0; j < k; ++j) {
+      const int s = t * k + j;
+      const int row = inv[s];
+      if (row < 0 || row >= T * k) continue;
+      add(load_slot<BY_SLOT>(y, s, row, H, c), s);
     }
   }
   if (OUT_FP32) {
@@ -56,6 +84,17 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(
   }
 }
 
+template <bool BY_SLOT, bool OUT_FP32>
+void launch_combine_k(dim3 grid, dim3 block, hipStream_t stream, const float* y,
+                      const int32_t* inv, const float* w, int T, int H, int k, void* out) {
+  if (k <= 8)
+    hipLaunchKernelGGL((combine_kernel<BY_SLOT, OUT_FP32, 8>), grid, block, 0, stream, y, inv, w,
+                       T, H, k, out);
+  else
+    hipLaunchKernelGGL((combine_kernel<BY_SLOT, OUT_FP32, 0>), grid, block, 0, stream, y, inv, w,
+                       T, H, k, out);
+}
+
 }  // namespace
 
 hipError_t launch_combine(const float* y, const int32_t* inv, const float* w,
@@ -64,11 +103,11 @@ hipError_t launch_combine(const float* y, const int32_t* inv, const float* w,
   if (T <= 0) return hipSuccess;
   const dim3 grid(T, (H + kCombineCols - 1) / kCombineCols), block(kCombineThreads);
   if (by_slot) {
-    if (out_fp32) hipLaunchKernelGGL((combine_kernel<true, true>), grid, block, 0, stream, y, inv, w, T, H, k, out);
-    else hipLaunchKernelGGL((combine_kernel<true, false>), grid, block, 0, stream, y, inv, w, T, H, k, out);
+    if (out_fp32) launch_combine_k<true, true>(grid, block, stream, y, inv, w, T, H, k, out);
+    else launch_combine_k<true, false>(grid, block, stream, y, inv, w, T, H, k, out);
   } else {
-    if (out_fp32) hipLaunchKernelGGL((combine_kernel<false, true>), grid, block, 0, stream, y, inv, w, T, H, k, out);
-    else hipLaunchKernelGGL((combine_kernel<false, false>), grid, block, 0, stream, y, inv, w, T, H, k, out);
+    if (out_fp32) launch_combine_k<false, true>(grid, block, stream, y, inv, w, T, H, k, out);
+    else launch_combine_k<false, false>(grid, block, stream, y, inv, w, T, H, k, out);
   }
   return hipGetLastError();
 }
