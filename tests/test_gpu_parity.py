@@ -454,6 +454,34 @@ def test_forward_1024_experts(gpu):
     check_close(got, ref["out"], "E=1024")
 
 
+TILE_EDGE_COUNTS = [1, 31, 32, 33, 63, 64, 65, 95, 96, 97, 127, 128, 129, 255, 256, 257, 0]
+
+
+@pytest.mark.parametrize("wdtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("H,extra", [(128, 0), (384, 0), (256, 3000)])
+def test_forward_tile_row_boundaries(gpu, wdtype, H, extra):
+    """Experts holding one row less than, exactly, and one row more than a
+    32-row block, a 96-row fp8 tile, a half (128-row) and a whole (256-row)
+    bf16 tile.  Without `extra` the batch is decode-sized (R <= 256 E: the
+    small-tile weight ring and the nontemporal weight reads); an extra expert
+    with `extra` rows makes it prefill-sized.  K = H gives 2, 6 and 4 K tiles."""
+    counts = TILE_EDGE_COUNTS + ([extra] if extra else [])
+    E, T, I = len(counts), int(sum(counts)), 128
+    rng = np.random.default_rng(40 + H + extra)
+    d = synth.make_inputs(T, H, I, E, 1, 41, zipf=None, wdtype=wdtype)
+    ids = np.repeat(np.arange(E, dtype=np.int32), counts)
+    d["topk_ids"] = rng.permutation(ids).reshape(T, 1).astype(np.int32)
+    d["topk_weights"] = np.ones((T, 1), dtype=np.float32)
+    say(f"tile edges {wdtype} H={H} extra={extra} T={T} E={E}")
+    ref = O.expert_forward(d)
+    assert np.array_equal(ref["routing"]["counts"], np.asarray(counts))
+    dev = to_device(d)
+    r = eaas.alloc_routing(T, 1, E)
+    got = forward(dev, 1, routing=r).cpu().numpy()
+    assert_routing_equal({key: v.cpu().numpy() for key, v in r.items()}, ref["routing"], T, E)
+    check_close(got, ref["out"], f"tile edges {wdtype} H={H}")
+
+
 def test_fp8_path_matches_bf16_on_representable_weights(gpu):
     d8 = synth.make_inputs(300, 512, 256, 4, 2, 35, wdtype="fp8")
     wgu, wdn = O.weights_f32(d8)
