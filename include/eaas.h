@@ -144,7 +144,7 @@ size_t eaas_workspace_bytes_for(const eaas_shape *s, int w_dtype, int entry);
  *   EAAS_WS_HS     its scales [R,I/128] fp32         (EAAS_FP8_E4M3_A8)
  *   EAAS_WS_XQ     x quantized [T,H] e4m3fn codes    (EAAS_FP8_E4M3_A8)
  *   EAAS_WS_XS     its scales [T,H/128] fp32         (EAAS_FP8_E4M3_A8)
- *   EAAS_WS_STAGE  weighted expert outputs [R,H] fp32, row = slot
+ *   EAAS_WS_STAGE  expert outputs [R,H] fp32 (not yet weighted), row = slot
  *                  t*k+j (eaas_expert_forward; invalid slots untouched)
  * Writes the byte offset and size of the region.  Returns INVALID_ARG for a
  * null output pointer, an unknown region or one the dtype does not have,

@@ -6,8 +6,9 @@
 // accumulated in fp32 from +0 with every product and sum rounded separately
 // (contraction into fused multiply-add is switched off in the kernel), so the
 // result does not depend on which entry point produced Y_s:
-//   rows_by_slot_weighted: y holds w[s] * Y_s already, at row s (fused step)
-//   otherwise:             y holds Y at row inv[s] (modular entry point)
+//   rows_by_slot: Y_s at row s (the fused step: the down projection's
+//                 epilogue stores each row at its slot)
+//   otherwise:    Y_s at row inv[s] (modular entry point, permuted order)
 // One workgroup per (token, 1024-column block); each thread owns 4
 // consecutive columns, and the staged rows are read once (non-temporal).
 #include "common.h"
@@ -19,8 +20,7 @@ namespace {
 constexpr int kCombineThreads = 256;
 constexpr int kCombineCols = kCombineThreads * 4;  // columns per workgroup
 
-// One slot's staged row: the weighted product already (BY_SLOT, at row s) or
-// the unweighted expert output (at row inv[s]).
+// One slot's staged row: at row s (BY_SLOT) or at row inv[s].
 template <bool BY_SLOT>
 __device__ __forceinline__ f32x4 load_slot(const float* __restrict__ y, int s, int row, int H,
                                            int c) {
@@ -30,8 +30,9 @@ __device__ __forceinline__ f32x4 load_slot(const float* __restrict__ y, int s, i
 }
 
 // grid: (T, ceil(H / kCombineCols)); each thread owns 4 consecutive columns.
-// KU > 0 (k <= KU): the k rows are all requested before the first add, so a
-// thread has k loads in flight; the adds still run in ascending j.
+// KU > 0 (k <= KU): the k rows and weights are all requested before the
+// first add, so a thread has k loads in flight; the adds still run in
+// ascending j.
 template <bool BY_SLOT, bool OUT_FP32, int KU>
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(
     const float* __restrict__ y, const int32_t* __restrict__ inv,
@@ -42,19 +43,14 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(
   const int c = blockIdx.y * kCombineCols + threadIdx.x * 4;
   if (c >= H) return;
   f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-  auto add = [&](const f32x4& v, int s) {
+  auto add = [&](const f32x4& v, float wj) {
 #pragma clang fp contract(off)
-    if (BY_SLOT) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc[q] = acc[q] + v[q];
-    } else {
-      const float wj = w[s];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) acc[q] = acc[q] + wj * v[q];
-    }
+    for (int q = 0; q < 4; ++q) acc[q] = acc[q] + wj * v[q];
   };
   if constexpr (KU > 0) {
     f32x4 v[KU];
+    float wv[KU];
     bool live[KU];
 #pragma unroll
     for (int j = 0; j < KU; ++j) {
@@ -62,16 +58,17 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(
       const int row = j < k ? inv[s] : -1;
       live[j] = row >= 0 && row < T * k;
       v[j] = live[j] ? load_slot<BY_SLOT>(y, s, row, H, c) : f32x4{};
+      wv[j] = live[j] ? w[s] : 0.0f;
     }
 #pragma unroll
     for (int j = 0; j < KU; ++j)
-      if (live[j]) add(v[j], t * k + j);
+      if (live[j]) add(v[j], wv[j]);
   } else {
     for (int j = 0; j < k; ++j) {
       const int s = t * k + j;
       const int row = inv[s];
       if (row < 0 || row >= T * k) continue;
-      add(load_slot<BY_SLOT>(y, s, row, H, c), s);
+      add(load_slot<BY_SLOT>(y, s, row, H, c), w[s]);
     }
   }
   if (OUT_FP32) {

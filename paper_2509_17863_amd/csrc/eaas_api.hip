@@ -255,7 +255,6 @@ int eaas_expert_ffn_grouped(const eaas_shape* s, const void* x, const eaas_routi
   set_dtype_args(a, w_dtype, base, L);
   a.h = reinterpret_cast<uint16_t*>(base + L.h);
   a.y = y_perm;
-  a.topk_weights = nullptr;
   a.epilogue = kDownPlain;
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   hipError_t e = quantize_x(a, base, L, hs);
@@ -327,8 +326,7 @@ int eaas_expert_forward_profiled(const eaas_shape* s, const void* x, const int32
   set_dtype_args(a, w_dtype, base, L);
   a.h = reinterpret_cast<uint16_t*>(base + L.h);
   a.y = stage;
-  a.topk_weights = topk_weights;
-  a.epilogue = kDownWeighted;
+  a.epilogue = kDownBySlot;
   // (fp8 activations: x is quantized in the routing interval, so the gate/up
   // interval times the GEMM alone)
   e = quantize_x(a, base, L, hs);
@@ -400,13 +398,12 @@ int eaas_expert_forward_segments(const eaas_shape* s, const eaas_segment* segs,
   set_dtype_args(a, w_dtype, base, L);
   a.h = reinterpret_cast<uint16_t*>(base + L.h);
   a.y = stage;
-  a.topk_weights = w_cat;
-  a.epilogue = kDownWeighted;
+  a.epilogue = kDownBySlot;
   e = quantize_x(a, base, L, hs);
   if (e == hipSuccess) e = launch_gate_up(a, hs);
   if (e == hipSuccess) e = launch_down(a, hs);
   if (e == hipSuccess)
-    e = launch_seg_combine(segs, num_tokens, n_seg, cap, s->H, s->k, stage, rt.inv,
+    e = launch_seg_combine(segs, num_tokens, n_seg, cap, s->H, s->k, stage, rt.inv, w_cat,
                            out_dtype == EAAS_FP32, hs);
   return hip_status(e);
 }
@@ -499,15 +496,14 @@ int eaas_server_step(const eaas_shape* s, const eaas_slot* slots, int n_slots,
     set_dtype_args(a, w_dtype, base, L);
     a.h = reinterpret_cast<uint16_t*>(base + L.h);
     a.y = reinterpret_cast<float*>(base + L.stage);
-    a.topk_weights = w_cat;
-    a.epilogue = kDownWeighted;
+    a.epilogue = kDownBySlot;
     a.layers = layers;
     a.e_layer = s->E;
     e = quantize_x(a, base, L, hs);
     if (e == hipSuccess) e = launch_gate_up(a, hs);
     if (e == hipSuccess) e = launch_down(a, hs);
     if (e == hipSuccess)
-      e = launch_seg_combine(segs, counts, n_slots, cap, g.H, g.k, a.y, rt.inv, false, hs);
+      e = launch_seg_combine(segs, counts, n_slots, cap, g.H, g.k, a.y, rt.inv, w_cat, false, hs);
     if (e != hipSuccess) return EAAS_ERR_HIP;
   }
   return hip_status(launch_slot_complete(slots, n_slots, taken, hs));

@@ -63,7 +63,7 @@ namespace {
 constexpr int kNumXcd = 8;
 constexpr int kGroupM = 4;  // M-tiles per ordering group inside an expert
 
-enum GemmKind { kGateUp = 0, kDownPlainK = 1, kDownWeightedK = 2 };
+enum GemmKind { kGateUp = 0, kDownPlainK = 1, kDownBySlotK = 2 };
 
 struct GemmParams {
   const uint16_t* a;      // gate/up: x [T, lda]; down: h [R, lda]
@@ -79,7 +79,6 @@ struct GemmParams {
   const int32_t* active;  // [E+1]
   uint16_t* h;            // gate/up output [R, I]
   float* y;               // down output [R, N]
-  const float* w;         // [R] router scores by slot
   int R;                  // slots (T*k)
   int E;                  // resident experts (groups)
   // server step over several layers: group e is expert e % e_layer of layer
@@ -336,7 +335,6 @@ __device__ __forceinline__ int block_row(int wn, int j) {
 template <int MBW>
 struct RowInfo {
   int orow[MBW];
-  float wt[MBW];
 };
 
 template <int KIND, int MBW>
@@ -349,11 +347,7 @@ __device__ __forceinline__ RowInfo<MBW> row_info(const GemmParams& p, const Tile
     const int rr = am0 + i * 32 + lrow;
     const int r = t.r0 + (rr < t.rows_valid ? rr : 0);
     ri.orow[i] = r;
-    ri.wt[i] = 1.0f;
-    if (KIND == kDownWeightedK && i < mb_live) {
-      ri.orow[i] = min(max(p.perm[r], 0), p.R - 1);
-      ri.wt[i] = p.w[ri.orow[i]];
-    }
+    if (KIND == kDownBySlotK && i < mb_live) ri.orow[i] = min(max(p.perm[r], 0), p.R - 1);
   }
   return ri;
 }
@@ -390,7 +384,6 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, const Tile& t, int
       }
     } else {
       const int orow = ri.orow[i];
-      const float wt = ri.wt[i];
       float* yrow = p.y + (size_t)orow * p.N + t.tn * BN + wn * NBW * 32;
 #pragma unroll
       for (int j = 0; j < NBW; ++j) {
@@ -399,10 +392,7 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, const Tile& t, int
           const int c = j * 32 + 8 * q + 4 * khalf;
           f32x4 v;
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const float a = acc[i][j][4 * q + u];
-            v[u] = KIND == kDownWeightedK ? wt * a : a;  // rounded product, stored
-          }
+          for (int u = 0; u < 4; ++u) v[u] = acc[i][j][4 * q + u];
           *reinterpret_cast<f32x4*>(yrow + c) = v;
         }
       }
@@ -445,17 +435,13 @@ __device__ __forceinline__ void epilogue_rows_lds(const GemmParams& p, const Til
 #pragma unroll
   for (int i = 0; i < MBW; ++i) {
     if (i >= mb_live) continue;
-    const float wt = ri.wt[i];
 #pragma unroll
     for (int j = 0; j < NBW; ++j) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         f32x4 v;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const float a = acc[i][j][4 * q + u];
-          v[u] = KIND == kDownWeightedK ? wt * a : a;  // rounded product, stored
-        }
+        for (int u = 0; u < 4; ++u) v[u] = acc[i][j][4 * q + u];
         *reinterpret_cast<LDS_AS f32x4*>(buf + lrow * LD + j * 32 + 8 * q + 4 * khalf) = v;
       }
     }
@@ -1674,17 +1660,12 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
     // stages 32 rows (two token blocks) at a time in its own LDS region and
     // stores whole 256-byte row segments
     int orow[MB];
-    float wt[MB];
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
       const int rr = am0 + i * 16 + l16;
       const int r = t.r0 + (rr < t.rows_valid ? rr : 0);
       orow[i] = r;
-      wt[i] = 1.0f;
-      if (KIND == kDownWeightedK && i < mb_live) {
-        orow[i] = min(max(p.perm[r], 0), p.R - 1);
-        wt[i] = p.w[orow[i]];
-      }
+      if (KIND == kDownBySlotK && i < mb_live) orow[i] = min(max(p.perm[r], 0), p.R - 1);
     }
     constexpr int COLS = NB * 16, LD = COLS + 4, LPR = COLS / 4, RPI = kWave / LPR;
     static_assert(8 * 32 * LD * 4 <= LDS_BYTES, "epilogue regions");
@@ -1703,7 +1684,7 @@ void grouped_gemm_w8a8_kernel(GemmParams p) {
           f32x4 v;
 #pragma unroll
           for (int u = 0; u < 4; ++u)
-            v[u] = KIND == kDownWeightedK ? wt[i] * acc[i][j][u] : acc[i][j][u];
+            v[u] = acc[i][j][u];
           *reinterpret_cast<LDS_AS f32x4*>(buf + (16 * h2 + l16) * LD + 16 * j + 4 * kq) = v;
         }
       }
@@ -1823,7 +1804,6 @@ GemmParams common_params(const FfnArgs& a) {
   g.offsets = a.offsets;
   g.active = a.active;
   g.I = a.I;
-  g.w = a.topk_weights;
   g.R = a.T * a.k;
   g.E = a.E;
   g.layers = a.layers;
@@ -1887,13 +1867,13 @@ hipError_t launch_down(const FfnArgs& a, hipStream_t stream) {
   if (a.act8) {
     g.a8 = a.hq;
     g.a_scale = a.hs;
-    return a.epilogue == kDownWeighted ? launch_w8a8<kDownWeightedK>(g, R, a.E, small_rows(a), stream)
-                                       : launch_w8a8<kDownPlainK>(g, R, a.E, small_rows(a), stream);
+    return a.epilogue == kDownBySlot ? launch_w8a8<kDownBySlotK>(g, R, a.E, small_rows(a), stream)
+                                     : launch_w8a8<kDownPlainK>(g, R, a.E, small_rows(a), stream);
   }
   const bool sm = small_rows(a);
-  if (a.epilogue == kDownWeighted)
-    return a.fp8 ? launch_kind<kDownWeightedK, true>(g, R, a.E, sm, stream)
-                 : launch_kind<kDownWeightedK, false>(g, R, a.E, sm, stream);
+  if (a.epilogue == kDownBySlot)
+    return a.fp8 ? launch_kind<kDownBySlotK, true>(g, R, a.E, sm, stream)
+                 : launch_kind<kDownBySlotK, false>(g, R, a.E, sm, stream);
   return a.fp8 ? launch_kind<kDownPlainK, true>(g, R, a.E, sm, stream)
                : launch_kind<kDownPlainK, false>(g, R, a.E, sm, stream);
 }

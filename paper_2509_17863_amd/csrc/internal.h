@@ -24,8 +24,8 @@ hipError_t launch_route_permute(const int32_t* ids, int R, int E,
 
 // Which epilogue the down projection uses.
 enum DownEpilogue {
-  kDownPlain = 0,     // y[r, :] = Y[r, :] (rows in permuted order)
-  kDownWeighted = 1,  // y[perm[r], :] = w[perm[r]] * Y[r, :] (rows by slot)
+  kDownPlain = 0,   // y[r, :] = Y[r, :] (rows in permuted order)
+  kDownBySlot = 1,  // y[perm[r], :] = Y[r, :] (rows by slot; the combine weights them)
 };
 
 struct FfnArgs {
@@ -41,7 +41,6 @@ struct FfnArgs {
   bool fp8;
   uint16_t* h;                // [R,I] bf16 scratch
   float* y;                   // [R,H] fp32
-  const float* topk_weights;  // [R] (weighted epilogue)
   int epilogue;               // DownEpilogue
   // server step over several layers: E = layers x e_layer groups whose weights
   // come from the per-layer records (w_* and s_* above are then unused)
@@ -75,14 +74,14 @@ hipError_t launch_gate_up(const FfnArgs& a, hipStream_t stream);
 // Down GEMM from h into y (epilogue per a.epilogue).
 hipError_t launch_down(const FfnArgs& a, hipStream_t stream);
 
-// out[t] = sum_j (weighted ? y[s] : w[s] * y[inv[s]]) over valid slots s = t*k+j.
+// out[t] = sum_j w[s] * y[by_slot ? s : inv[s]] over valid slots s = t*k+j.
 hipError_t launch_combine(const float* y, const int32_t* inv, const float* w,
-                          int T, int H, int k, bool rows_by_slot_weighted,
+                          int T, int H, int k, bool rows_by_slot,
                           void* out, bool out_fp32, hipStream_t stream);
 
 // Dynamic batch (Algorithm 1 walks): gather the requests' tokens into the
 // contiguous batch of `cap` rows (slots of unused capacity get id -1), and
-// write each request's weighted sums from the by-slot fp32 staging rows.
+// write each request's weighted sums of the by-slot fp32 staging rows.
 // id_off (optional): per request, the group offset of its ids (valid ids are
 // those in [0, e_local)); a negative offset masks the request's slots.
 hipError_t launch_seg_gather(const eaas_segment* segs, const int32_t* num_tokens, int n_seg,
@@ -91,7 +90,7 @@ hipError_t launch_seg_gather(const eaas_segment* segs, const int32_t* num_tokens
                              hipStream_t stream);
 hipError_t launch_seg_combine(const eaas_segment* segs, const int32_t* num_tokens, int n_seg,
                               int cap, int H, int k, const float* stage, const int32_t* inv,
-                              bool out_fp32, hipStream_t stream);
+                              const float* w, bool out_fp32, hipStream_t stream);
 
 // Server step: snapshot the slots into a dynamic batch (records, counts,
 // layer group offsets, taken mask), and mark the taken slots done.

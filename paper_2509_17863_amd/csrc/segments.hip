@@ -14,8 +14,8 @@
 //   seg_gather:  token g of the batch -> row g of the contiguous batch
 //                (hidden state, expert ids, router scores); slots of the
 //                unused capacity get id -1, so the routing skips them
-//   seg_combine: out_b[t] = sum over ascending j of the staged weighted rows
-//                of slots g*k+j, in fp32 from +0 without fused multiply-add:
+//   seg_combine: out_b[t] = sum over ascending j of w[s] times the staged row
+//                of slot s = g*k+j, in fp32 from +0 without fused multiply-add:
 //                bitwise what the single-batch combine writes for token g
 #include "common.h"
 #include "internal.h"
@@ -80,7 +80,8 @@ __global__ __launch_bounds__(kSegThreads) void seg_gather_kernel(
 template <bool OUT_FP32>
 __global__ __launch_bounds__(kSegThreads) void seg_combine_kernel(
     const eaas_segment* __restrict__ segs, const int32_t* __restrict__ num_tokens, int n_seg,
-    int cap, int H, int k, const float* __restrict__ stage, const int32_t* __restrict__ inv) {
+    int cap, int H, int k, const float* __restrict__ stage, const int32_t* __restrict__ inv,
+    const float* __restrict__ w) {
   // products and sums are rounded separately: no fused multiply-add here
 #pragma clang fp contract(off)
   __shared__ int s_n[kMaxSegments];
@@ -100,8 +101,9 @@ __global__ __launch_bounds__(kSegThreads) void seg_combine_kernel(
             if (inv[s] < 0) continue;
             const f32x4 v = __builtin_nontemporal_load(
                 reinterpret_cast<const f32x4*>(stage + s * H + c));
+            const float ws = w[s];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) acc[q] = acc[q] + v[q];
+            for (int q = 0; q < 4; ++q) acc[q] = acc[q] + ws * v[q];
           }
           if (OUT_FP32) {
             *reinterpret_cast<f32x4*>(static_cast<float*>(out) + (size_t)token_id * H + c) = acc;
@@ -214,13 +216,13 @@ hipError_t launch_slot_complete(const eaas_slot* slots, int n_slots, const int32
 
 hipError_t launch_seg_combine(const eaas_segment* segs, const int32_t* num_tokens, int n_seg,
                               int cap, int H, int k, const float* stage, const int32_t* inv,
-                              bool out_fp32, hipStream_t stream) {
+                              const float* w, bool out_fp32, hipStream_t stream) {
   if (out_fp32)
     hipLaunchKernelGGL((seg_combine_kernel<true>), dim3(seg_grid(cap)), dim3(kSegThreads), 0,
-                       stream, segs, num_tokens, n_seg, cap, H, k, stage, inv);
+                       stream, segs, num_tokens, n_seg, cap, H, k, stage, inv, w);
   else
     hipLaunchKernelGGL((seg_combine_kernel<false>), dim3(seg_grid(cap)), dim3(kSegThreads), 0,
-                       stream, segs, num_tokens, n_seg, cap, H, k, stage, inv);
+                       stream, segs, num_tokens, n_seg, cap, H, k, stage, inv, w);
   return hipGetLastError();
 }
 
