@@ -1,8 +1,8 @@
 """Benchmark of one expert server's forward step on one MI355X.
 
 A step is one eaas_expert_forward over one batch of the named synthetic
-workload (routing, grouped gate/up GEMM + SiLU*mul, grouped down GEMM with the
-weighted epilogue, combine), inputs resident in HBM.  Prints one JSON line.
+workload (routing, grouped gate/up GEMM + SiLU*mul, grouped down GEMM into
+by-slot rows, weighted combine), inputs resident in HBM.  Prints one JSON line.
 """
 from __future__ import annotations
 
