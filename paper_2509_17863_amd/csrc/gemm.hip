@@ -5,7 +5,8 @@
 //   gate/up:  C[r, n] = x[perm[r]/k, :] . W_gate_up[e][n, :]   (rows gathered)
 //             epilogue h[r, c] = bf16(silu(C_gate[r, c]) * C_up[r, c])
 //   down:     C[r, n] = h[r, :] . W_down[e][n, :]
-//             epilogue y[perm[r], n] = w[perm[r]] * C (fp32, rows by slot) or
+//             epilogue y[perm[r], n] = C (fp32, rows by slot; the combine
+//                      applies the router weights) or
 //                      y[r, n] = C (fp32, rows in permuted order)
 //
 // A tile is BM token rows x BN weight rows.  Each of the WM x WN waves owns
@@ -407,8 +408,8 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, const Tile& t, int
 // the tile's last K tiles.  Here each wave passes its accumulators, one
 // 32-row block at a time, through a private LDS region and stores whole
 // rows of its columns: with NBW = 2 one instruction writes 4 rows x 256
-// contiguous bytes.  The values stored are those of `epilogue` (the same
-// rounded product w * a, or a), bit for bit.  Every wave must have finished
+// contiguous bytes.  The values stored are those of `epilogue` (the fp32
+// accumulators), bit for bit.  Every wave must have finished
 // the main loop's LDS reads (and its DMA must have landed) before any wave
 // calls this: the callers reach it after the loop's last barrier.
 template <int NBW>
