@@ -39,6 +39,10 @@ def shape(T=64, H=256, I=128, E=8, k=2):
     (dict(), True), (dict(T=0), True), (dict(H=200), False), (dict(I=100), False),
     (dict(E=0), False), (dict(E=1025), False), (dict(k=0), False), (dict(k=65), False),
     (dict(T=-1), False), (dict(T=1 << 28, k=8), False),
+    # 32-bit element offsets in the kernels: T*H, T*k*I and 4*I*H stay <= INT_MAX
+    (dict(T=(1 << 24) - 1, H=128, I=128, k=1), True), (dict(T=1 << 24, H=128, I=128, k=1), False),
+    (dict(T=(1 << 23) - 1, H=128, I=256, k=1), True), (dict(T=1 << 23, H=128, I=256, k=1), False),
+    (dict(T=4, H=23168, I=23168), True), (dict(T=4, H=23168, I=23296), False),
 ])
 def test_workspace_bytes_validation(kw, ok):
     s = shape(**kw)
