@@ -69,7 +69,8 @@ enum eaas_status {
   EAAS_ERR_INVALID_ARG = -1, /* null pointer, negative size, bad dtype, overlap
                                 (k > E is valid: see eaas_route_permute) */
   EAAS_ERR_UNSUPPORTED = -2, /* H or I not a multiple of 128, E > 1024, k > 64,
-                                T*k >= 2^31 or sizes past 32-bit row indexing */
+                                or past the 32-bit element offsets the kernels
+                                use: T*k, T*H, T*k*I or 4*I*H above 2^31 - 1 */
   EAAS_ERR_WORKSPACE = -3,   /* ws NULL, misaligned or smaller than the entry
                                 point's eaas_workspace_bytes_for */
   EAAS_ERR_HIP = -4          /* a kernel launch was rejected by the runtime  */

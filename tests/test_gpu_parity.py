@@ -482,6 +482,40 @@ def test_forward_tile_row_boundaries(gpu, wdtype, H, extra):
     check_close(got, ref["out"], f"tile edges {wdtype} H={H}")
 
 
+@pytest.mark.parametrize("wdtype", ["bf16", "fp8"])
+def test_forward_at_the_32bit_offset_limit(gpu, wdtype):
+    """The largest batch the 32-bit element offsets allow at H = 1024:
+    T*H = 2^31 - 1024 (x is 4 GiB, so the DMA's byte offsets into it reach
+    2^32 - 2048).  Routing against a stable sort on every slot; the output of
+    the first, middle and last tokens against the oracle."""
+    T, H, I, E, k = (1 << 21) - 1, 1024, 128, 4, 2
+    say(f"offset limit {wdtype} T={T} H={H}")
+    dw = synth.make_inputs(1, H, I, E, k, 44, wdtype=wdtype)
+    g = torch.Generator(device="cuda").manual_seed(45)
+    x = torch.randn(T, H, generator=g, device="cuda").to(torch.bfloat16)
+    e0 = torch.randint(0, E, (T,), generator=g, device="cuda")
+    e1 = (e0 + torch.randint(1, E, (T,), generator=g, device="cuda")) % E
+    ids = torch.stack([e0, e1], 1).to(torch.int32).contiguous()
+    w = torch.rand(T, k, generator=g, device="cuda") + 0.1
+    w = (w / w.sum(1, keepdim=True)).contiguous()
+    dev = dict(to_device(dw), x=x, topk_ids=ids, topk_weights=w)
+    r = eaas.alloc_routing(T, k, E)
+    out = forward(dev, k, routing=r)
+    torch.cuda.synchronize()
+    flat = ids.flatten().to(torch.int64)
+    assert torch.equal(r["counts"][:E].to(torch.int64), torch.bincount(flat, minlength=E))
+    assert torch.equal(r["perm"][:T * k].to(torch.int64), torch.argsort(flat, stable=True))
+    idx = np.r_[0:16, T // 2 - 8:T // 2 + 8, T - 32:T]
+    ti = torch.from_numpy(idx).cuda()
+    ds = dict(dw, T=len(idx), x=bf16_tensor_to_bits(x[ti]), topk_ids=ids[ti].cpu().numpy(),
+              topk_weights=w[ti].cpu().numpy())
+    ref = O.expert_forward(ds)
+    got = out[ti].cpu().numpy()
+    del out, x, dev, r
+    torch.cuda.empty_cache()
+    check_close(got, ref["out"], f"offset limit {wdtype}")
+
+
 def test_fp8_path_matches_bf16_on_representable_weights(gpu):
     d8 = synth.make_inputs(300, 512, 256, 4, 2, 35, wdtype="fp8")
     wgu, wdn = O.weights_f32(d8)
