@@ -482,15 +482,19 @@ def test_forward_tile_row_boundaries(gpu, wdtype, H, extra):
     check_close(got, ref["out"], f"tile edges {wdtype} H={H}")
 
 
-@pytest.mark.parametrize("wdtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("wdtype", ["bf16", "fp8", "a8"])
 def test_forward_at_the_32bit_offset_limit(gpu, wdtype):
     """The largest batch the 32-bit element offsets allow at H = 1024:
     T*H = 2^31 - 1024 (x is 4 GiB, so the DMA's byte offsets into it reach
     2^32 - 2048).  Routing against a stable sort on every slot; the output of
-    the first, middle and last tokens against the oracle."""
+    the first, middle and last tokens against the oracle (fp8 activations:
+    its RMS error, as for the random shapes)."""
+    from oracle import w8a8_oracle as W
+
     T, H, I, E, k = (1 << 21) - 1, 1024, 128, 4, 2
+    act8 = wdtype == "a8"
     say(f"offset limit {wdtype} T={T} H={H}")
-    dw = synth.make_inputs(1, H, I, E, k, 44, wdtype=wdtype)
+    dw = synth.make_inputs(1, H, I, E, k, 44, wdtype="bf16" if wdtype == "bf16" else "fp8")
     g = torch.Generator(device="cuda").manual_seed(45)
     x = torch.randn(T, H, generator=g, device="cuda").to(torch.bfloat16)
     e0 = torch.randint(0, E, (T,), generator=g, device="cuda")
@@ -500,7 +504,15 @@ def test_forward_at_the_32bit_offset_limit(gpu, wdtype):
     w = (w / w.sum(1, keepdim=True)).contiguous()
     dev = dict(to_device(dw), x=x, topk_ids=ids, topk_weights=w)
     r = eaas.alloc_routing(T, k, E)
-    out = forward(dev, k, routing=r)
+    if act8:
+        ws = eaas.alloc_workspace(T, H, I, E, k, eaas.EAAS_FP8_E4M3_A8)
+        out = torch.full((T, H), float("nan"), dtype=torch.float32, device="cuda")
+        eaas.eaas_expert_forward(x, ids, w, dev["w_gate_up"], dev["w_down"], out, ws,
+                                 dev["w_gate_up_scale"], dev["w_down_scale"], routing=r,
+                                 act8=True)
+        del ws
+    else:
+        out = forward(dev, k, routing=r)
     torch.cuda.synchronize()
     flat = ids.flatten().to(torch.int64)
     assert torch.equal(r["counts"][:E].to(torch.int64), torch.bincount(flat, minlength=E))
@@ -509,11 +521,17 @@ def test_forward_at_the_32bit_offset_limit(gpu, wdtype):
     ti = torch.from_numpy(idx).cuda()
     ds = dict(dw, T=len(idx), x=bf16_tensor_to_bits(x[ti]), topk_ids=ids[ti].cpu().numpy(),
               topk_weights=w[ti].cpu().numpy())
-    ref = O.expert_forward(ds)
     got = out[ti].cpu().numpy()
     del out, x, dev, r
     torch.cuda.empty_cache()
-    check_close(got, ref["out"], f"offset limit {wdtype}")
+    if act8:
+        ref = W.expert_forward_w8a8(ds)["out"]
+        rms = float(np.sqrt((ref ** 2).mean()))
+        err = float(np.sqrt(((got.astype(np.float64) - ref) ** 2).mean()))
+        say(f"offset limit a8: rms_err={err:.3e} rms={rms:.3e}")
+        assert np.isfinite(got).all() and err <= TOL * rms
+    else:
+        check_close(got, O.expert_forward(ds)["out"], f"offset limit {wdtype}")
 
 
 def test_fp8_path_matches_bf16_on_representable_weights(gpu):
